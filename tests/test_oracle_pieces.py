@@ -1,0 +1,210 @@
+"""Pins for the oracle's building blocks: schedule, DDIM coefficients, bf16 rounding,
+patchify, time embedding, GELU, the two networks. CPU only."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import eps_models as em
+from oracle import sampler as sp
+from oracle import schedule as sch
+from paper_2609_36522_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+# ----------------------------------------------------------------------------- schedule
+def test_schedule_endpoints_and_sqrt_linearity():
+    g = _golden("schedule_closed_form.json")
+    abar = sch.scaled_linear_alpha_bar()
+    assert abar.shape == (1000,)
+    # alpha_bar_0 = 1 - beta_0 exactly; betas recovered from the ratio are the endpoints.
+    assert abar[0] == pytest.approx(g["alpha_bar_0"], abs=1e-15)
+    beta = np.empty(1000)
+    beta[0] = 1 - abar[0]
+    beta[1:] = 1 - abar[1:] / abar[:-1]
+    assert beta[0] == pytest.approx(g["beta_start"], rel=1e-12)
+    assert beta[-1] == pytest.approx(g["beta_end"], rel=1e-9)
+    # sqrt(beta) is an arithmetic progression: second differences vanish.
+    sb = np.sqrt(beta)
+    assert np.max(np.abs(np.diff(sb, 2))) < 1e-10
+    assert np.all(np.diff(abar) < 0)
+
+
+@pytest.mark.parametrize("T", [10, 50, 100, 1000])
+def test_trailing_timesteps_closed_form(T):
+    g = _golden("schedule_closed_form.json")
+    t = sch.trailing_timesteps(T)
+    exp = g["trailing"][str(T)]
+    assert t[0] == exp["first"] and t[-1] == exp["last"]
+    assert np.all(np.diff(t) == -exp["stride"])
+    assert len(t) == T
+
+
+def test_ddim_coefficients_exact_for_true_noise():
+    """With eps(x) = n (the true noise) and x_0 = sqrt(ab_0) x0 + sqrt(1-ab_0) n, deterministic
+    DDIM reproduces sqrt(ab_i) x0 + sqrt(1-ab_i) n at every step, so x_T = x0 (ab_T = 1)."""
+    rng = np.random.default_rng(5)
+    T = 25
+    ab, t = sch.sampler_alpha_bar(T)
+    alpha, b = sch.ddim_coefficients(ab)
+    x0 = rng.standard_normal(64)
+    n = rng.standard_normal(64)
+    xi = np.sqrt(ab[0]) * x0 + np.sqrt(1 - ab[0]) * n
+    const = lambda X, steps: np.repeat(n[None, :], len(steps), axis=0).astype(X.dtype)
+    x_drift = sp.ddim_serial_drift(xi, alpha, b, const, store_dtype=np.float64)
+    x_text = sp.ddim_serial_textbook(xi, ab, const, store_dtype=np.float64)
+    assert np.max(np.abs(x_drift - x0)) < 1e-12
+    assert np.max(np.abs(x_text - x0)) < 1e-12
+    # Coefficient signs: ab increases along the sampler, so a_i > 1 and b_i < 0.
+    assert np.all(alpha > 0) and np.all(b < 0)
+
+
+def test_ddim_drift_equals_textbook_for_state_dependent_eps():
+    rng = np.random.default_rng(6)
+    T = 10
+    ab, _ = sch.sampler_alpha_bar(T)
+    alpha, b = sch.ddim_coefficients(ab)
+    c = rng.uniform(0.5, 1.5, T)
+    x = rng.standard_normal(32)
+    e = em.linear_eps(c)
+    d = sp.ddim_serial_drift(x, alpha, b, e, store_dtype=np.float64)
+    tb = sp.ddim_serial_textbook(x, ab, e, store_dtype=np.float64)
+    assert np.max(np.abs(d - tb)) <= 1e-12 * np.max(np.abs(tb))
+
+
+# ----------------------------------------------------------------------------- bf16
+def test_bf16_round_known_values():
+    one = np.float32(1.0)
+    ulp = np.float32(2.0 ** -7)          # bf16 spacing at 1.0
+    vals = np.array([1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, 1 + 2 ** -8 + 2 ** -20, -2.5,
+                     0.0, np.inf], dtype=np.float32)
+    exp = np.array([1.0, 1.0, 1 + 2 * ulp, 1 + ulp, -2.5, 0.0, np.inf], dtype=np.float32)
+    got = em.bf16_round(vals)
+    assert np.array_equal(got, exp)
+    assert np.isnan(em.bf16_round(np.array([np.nan], np.float32))[0])
+    assert one == em.bf16_round(np.array([one]))[0]
+
+
+def test_bf16_round_matches_torch():
+    rng = np.random.default_rng(7)
+    x = (rng.standard_normal(100000) * 10.0 ** rng.integers(-6, 6, 100000)).astype(np.float32)
+    # add exact ties
+    ties = (np.arange(1, 2000, dtype=np.uint32) << 16 | 0x8000).view(np.float32)
+    x = np.concatenate([x, ties, -ties])
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(em.bf16_round(x), ref)
+
+
+def test_input_weights_are_bf16_of_normal_draws():
+    w = inputs.mlp_weights(64)
+    assert w["w1"].shape == (16, 64) and w["wt"].shape == (128, 64)
+    assert w["w2"].shape == (64, 64) and w["w3"].shape == (64, 16)
+    v = em.bf16_bits_to_f64(w["w2"])
+    assert abs(np.std(v) - 1 / 8) < 0.01
+    # same draws reproduced independently: fp32 normal / sqrt(fan_in), rounded by torch
+    rng = np.random.default_rng(inputs.SEED_WEIGHTS)
+    w1 = (rng.standard_normal((16, 64)) / 4.0).astype(np.float32)
+    ref = torch.from_numpy(w1).to(torch.bfloat16).to(torch.float32).numpy().astype(np.float64)
+    assert np.array_equal(em.bf16_bits_to_f64(w["w1"]), ref)
+
+
+# ----------------------------------------------------------------------------- patchify
+def test_patchify_index_formula_brute_force():
+    C, H, W, p = 4, 6, 10, 2
+    x = np.arange(C * H * W, dtype=np.float32).reshape(C, H, W)
+    tok = em.patchify(x, p)
+    assert tok.shape == ((H // p) * (W // p), C * p * p)
+    for h in range(H):
+        for w in range(W):
+            for c in range(C):
+                token = (h // p) * (W // p) + (w // p)
+                feat = c * p * p + (h % p) * p + (w % p)
+                assert tok[token, feat] == x[c, h, w]
+    assert np.array_equal(em.unpatchify(tok, (C, H, W), p), x)
+
+
+# ----------------------------------------------------------------------------- temb, GELU
+def test_timestep_embedding_closed_form():
+    e = em.timestep_embedding([0.0, 1.0, 999.0], 128)
+    assert np.array_equal(e[0, :64], np.zeros(64)) and np.array_equal(e[0, 64:], np.ones(64))
+    assert e[1, 0] == pytest.approx(math.sin(1.0), abs=1e-15)
+    assert e[1, 64] == pytest.approx(math.cos(1.0), abs=1e-15)
+    w63 = math.exp(-math.log(10000.0) * 63 / 64)
+    assert e[2, 63] == pytest.approx(math.sin(999.0 * w63), abs=1e-13)
+    assert e[2, 127] == pytest.approx(math.cos(999.0 * w63), abs=1e-13)
+
+
+def test_gelu_against_math_erf():
+    rng = np.random.default_rng(8)
+    x = np.concatenate([rng.standard_normal(2000) * 4, [0.0, -10.0, 10.0, 1e-30]])
+    ref = np.array([0.5 * v * (1.0 + math.erf(v / math.sqrt(2.0))) for v in x])
+    assert np.max(np.abs(em.gelu(x) - ref)) < 1e-15
+    assert em.gelu(np.array([0.0]))[0] == 0.0
+
+
+# ----------------------------------------------------------------------------- networks
+def test_linear_eps_is_fp32_product():
+    rng = np.random.default_rng(9)
+    c = rng.uniform(0.5, 1.5, 5).astype(np.float32)
+    X = rng.standard_normal((3, 100)).astype(np.float32)
+    out = em.linear_eps(c)(X, [0, 3, 4])
+    ref = np.stack([c[0] * X[0], c[3] * X[1], c[4] * X[2]])   # numpy fp32 multiply
+    assert out.dtype == np.float32 and np.array_equal(out, ref)
+
+
+def _mlp_explicit(x, j, w, t_values, shape):
+    """Explicit-loop patch-MLP on tiny shapes: per token, per unit, math.erf GELU."""
+    C, H, W = shape
+    W1, Wt, W2, W3 = (em.bf16_bits_to_f64(w[k]) for k in ("w1", "wt", "w2", "w3"))
+    hid = W1.shape[1]
+    half = Wt.shape[0] // 2
+    t = float(t_values[j])
+    temb = [math.sin(t * math.exp(-math.log(1e4) * k / half)) for k in range(half)] + \
+           [math.cos(t * math.exp(-math.log(1e4) * k / half)) for k in range(half)]
+    e = [np.float32(sum(temb[k] * Wt[k, n] for k in range(2 * half))) for n in range(hid)]
+    gelu = lambda v: 0.5 * v * (1.0 + math.erf(v / math.sqrt(2.0)))
+    bf = lambda v: float(em.bf16_round(np.array([np.float32(v)]))[0])
+    xs = x.reshape(shape)
+    out = np.zeros(shape, np.float32)
+    for hp in range(H // 2):
+        for wp in range(W // 2):
+            feats = [bf(xs[c, 2 * hp + dh, 2 * wp + dw]) for c in range(C) for dh in (0, 1) for dw in (0, 1)]
+            h1 = []
+            for n in range(hid):
+                pre = np.float32(sum(feats[f] * W1[f, n] for f in range(16)) + float(e[n]))
+                h1.append(bf(np.float32(gelu(float(pre)))))
+            h2 = []
+            for n in range(hid):
+                pre = np.float32(sum(h1[k] * W2[k, n] for k in range(hid)))
+                h2.append(bf(np.float32(gelu(float(pre)))))
+            for f in range(16):
+                v = np.float32(sum(h2[n] * W3[n, f] for n in range(hid)))
+                c, dh, dw = f // 4, (f // 2) % 2, f % 2
+                out[c, 2 * hp + dh, 2 * wp + dw] = v
+    return out.reshape(-1)
+
+
+def test_patch_mlp_matches_explicit_loops():
+    shape = (4, 4, 6)
+    hid = 24
+    w = inputs.mlp_weights(hid)
+    _, t_values = sch.sampler_alpha_bar(7)
+    net = em.PatchMLP(w, t_values, shape)
+    x = inputs.x_init(shape, seed=11).reshape(-1)
+    for j in (0, 4):
+        got = net(x[None, :], [j])[0]
+        ref = _mlp_explicit(x, j, w, t_values, shape)
+        scale = np.sqrt(np.mean(ref.astype(np.float64) ** 2))
+        # Same operands, same bf16 rounding points; only fp64 summation order differs, which
+        # can flip a rare bf16 rounding: allow a few bf16 steps of one activation.
+        assert np.max(np.abs(got - ref)) <= 2e-3 * scale
+        assert np.mean(got == ref) > 0.9
