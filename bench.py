@@ -1,0 +1,188 @@
+"""Benchmark of the cached Picard sampler on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+
+Workload: the SD-latent patch-MLP case (latent 4x64x64, T = 100 DDIM steps, window 32,
+hidden 1024 over 1024 tokens, tau = 1e-3), synthetic seeded inputs already resident in HBM.
+One step = one complete sample (every sweep until the window reaches T) through the C ABI.
+value = sweeps/s at delta = 0.05; eps evals/s and NFE saved against delta = 0 are reported
+beside it, as are the other cache tolerances of the sweep {0, 0.02, 0.05, 0.1}.
+
+Prints one JSON line (rank 0). The roofline object describes the dominant kernel (the fused
+patch-MLP network kernel): achieved = algorithmic FLOPs of its launches / their summed
+duration, timed with HIP events on the sampler's stream inside the timed region.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "cached Picard sweeps/s + ε evals/s at 4×64×64, T=100; NFE saved vs δ=0"
+PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
+PRIMARY_DELTA = 0.05
+
+
+def flops_per_eval(wl) -> float:
+    """Algorithmic FLOPs of one patch-MLP evaluation: 2 * tokens * (16 H + H^2 + 16 H)."""
+    H = wl.hidden
+    return 2.0 * wl.tokens * (16 * H + H * H + 16 * H)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--deltas", type=str, default="0,0.02,0.05,0.1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the oracle's bounded sample")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (counter calibration)")
+    return ap.parse_args()
+
+
+def timed_samples(sampler, x, steps, warmup, torch):
+    out = torch.empty_like(x)
+    for _ in range(warmup):                         # untimed warm-up generations
+        sampler.sample(x, out)
+    torch.cuda.synchronize()
+    sweeps = nfe = hits = 0
+    eps_ms = 0.0
+    launches = 0
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        sampler.sample(x, out)
+        st = sampler.stats()
+        kt = sampler.kernel_times()
+        sweeps += st["sweeps"]
+        nfe += st["nfe"]
+        hits += st["hits"]
+        eps_ms += kt["eps_ms_total"]
+        launches += kt["launches"]
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    return {"seconds": dt, "sweeps": sweeps, "nfe": nfe, "hits": hits, "eps_ms": eps_ms,
+            "launches": launches, "out": out}
+
+
+def cpu_baseline(wl, delta, budget_s):
+    """The oracle (as it stands) on a bounded prefix of the same sample."""
+    import numpy as np
+    from oracle import eps_models as em
+    from oracle import sampler as sp
+    from oracle import schedule as sch
+    from paper_2609_36522_amd import inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    ab, t = sch.sampler_alpha_bar(wl.T)
+    alpha, b = sch.ddim_coefficients(ab)
+    net = em.PatchMLP(inputs.mlp_weights(wl.hidden, temb_dim=wl.temb_dim), t, wl.latent)
+    st = sp.init_state(inputs.x_init(wl.latent), wl.T)
+    t0 = time.perf_counter()
+    while not st.done and time.perf_counter() - t0 < budget_s:
+        sp.sweep(st, wl.window, delta, wl.tol, alpha, b, net)
+    dt = time.perf_counter() - t0
+    return {"value": st.sweeps / dt, "unit": "sweeps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {st.sweeps} sweeps (NFE {st.nfe}, {dt:.1f} s) of the delta={delta} "
+                      f"sample, float64 NumPy oracle",
+            "eps_evals_per_s": st.nfe / dt}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); the sampler has no "
+              f"multi-GPU path in this build.", file=sys.stderr, flush=True)
+        sys.exit(2)
+    import torch
+    from paper_2609_36522_amd import binding, inputs, workloads
+
+    binding.load_library()
+    torch.cuda.set_device(0)
+    wl = workloads.SD_MLP
+    deltas = [float(v) for v in args.deltas.split(",")]
+    if PRIMARY_DELTA not in deltas:
+        deltas.append(PRIMARY_DELTA)
+    x = torch.from_numpy(inputs.x_init(wl.latent).reshape(-1)).cuda()
+    weights = inputs.mlp_weights(wl.hidden, temb_dim=wl.temb_dim)
+    fpe = flops_per_eval(wl)
+
+    per_delta = {}
+    for d in deltas:
+        with binding.from_workload(wl, d, seed_weights=weights, profile=True) as s:
+            r = timed_samples(s, x, args.steps, args.warmup, torch)
+        per_delta[d] = r
+        print(f"[bench] delta={d}: {r['sweeps'] / args.steps:.1f} sweeps/sample, "
+              f"NFE {r['nfe'] / args.steps:.1f}, {1e3 * r['seconds'] / args.steps:.3f} ms/sample",
+              file=sys.stderr, flush=True)
+
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, device="cuda")
+        bb = torch.empty_like(a)
+        for _ in range(3):
+            bb.copy_(a)
+        torch.cuda.synchronize()
+
+    p = per_delta[PRIMARY_DELTA]
+    d0 = per_delta.get(0.0)
+    sweeps_per_s = p["sweeps"] / p["seconds"]
+    eps_per_s = p["nfe"] / p["seconds"]
+    achieved = (p["nfe"] * fpe) / (p["eps_ms"] * 1e-3) / 1e12 if p["eps_ms"] > 0 else 0.0
+    line = {
+        "metric": METRIC,
+        "value": sweeps_per_s,
+        "unit": "sweeps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * p["seconds"] / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "latent": list(wl.latent), "T": wl.T,
+                   "window": wl.window, "delta": PRIMARY_DELTA, "tau": wl.tol,
+                   "eps_net": f"patch-MLP 16-{wl.hidden}-{wl.hidden}-16 bf16 MFMA, fp32 state",
+                   "tokens": wl.tokens, "step": "one full sample (all sweeps until done)",
+                   "parallelism": "single GPU"},
+        "eps_evals_per_s": eps_per_s,
+        "nfe_per_sample": p["nfe"] / args.steps,
+        "hits_per_sample": p["hits"] / args.steps,
+        "sweeps_per_sample": p["sweeps"] / args.steps,
+        "nfe_saved_vs_delta0": (1.0 - p["nfe"] / d0["nfe"]) if d0 else None,
+        "per_delta": {str(d): {"sweeps_per_s": r["sweeps"] / r["seconds"],
+                               "eps_evals_per_s": r["nfe"] / r["seconds"],
+                               "ms_per_sample": 1e3 * r["seconds"] / args.steps,
+                               "nfe_per_sample": r["nfe"] / args.steps,
+                               "hits_per_sample": r["hits"] / args.steps,
+                               "sweeps_per_sample": r["sweeps"] / args.steps,
+                               "nfe_saved_vs_delta0": (1.0 - r["nfe"] / d0["nfe"]) if d0 else None,
+                               "eps_kernel_tflops": ((r["nfe"] * fpe) / (r["eps_ms"] * 1e-3) / 1e12
+                                                     if r["eps_ms"] > 0 else None)}
+                      for d, r in per_delta.items()},
+        "roofline": {"bound": "mfma", "kernel": "k_eps_mlp<1024>",
+                     "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "avg_launch_us": 1e3 * p["eps_ms"] / max(p["launches"], 1),
+                     "flops_per_launch": p["nfe"] * fpe / max(p["launches"], 1)},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, PRIMARY_DELTA, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,200 @@
+/*
+ * paraanya.h — C ABI of the MI355X (gfx950) cached Picard sliding-window sampler.
+ *
+ * The sampler is the output-cached parallel-in-time diffusion sampler of
+ * "ParaAnya: Accelerating Parallel Diffusion Sampling with Plug-and-Play Output
+ * Caching": Picard iteration over a sliding window of P timesteps (Sec. 2.1, Eq. (1),
+ * convergence test Eq. (2)) with an output cache in front of the noise network
+ * (Sec. 2.2, Eq. (3)-(7)). One sweep on the device is:
+ *   (1) per-timestep cache test, mean |x_t - x^_t| < delta        (Eq. (4), (5));
+ *   (2) compaction of the misses into a dense batch                 (Eq. (5));
+ *   (3) one batched network evaluation of the misses only           (Sec. 2.2);
+ *   (4) scatter of the fresh outputs into the cache                 (Eq. (6), (7));
+ *   (5) DDIM drift at the current latents and the Picard prefix sum
+ *       anchored at the window start                                (Eq. (1));
+ *   (6) residuals, convergence test against tau, window slide       (Eq. (2)).
+ *
+ * Conventions
+ *   - All entry points return PA_OK (0) or a negative PA_ERR_* code; no C++ exception
+ *     crosses this boundary. paraanya_last_error() gives a thread-local message.
+ *   - One handle = one HIP stream (given at create). Every device operation of the
+ *     handle is enqueued on that stream. A handle is not thread-safe.
+ *   - Device pointers are HIP device addresses on the handle's current device; host
+ *     pointers are ordinary CPU memory. The library never takes ownership of caller
+ *     memory: it copies what it needs and owns every buffer it allocates.
+ *   - Latents are fp32, batch 1, layout [C][H][W] row-major, D = C*H*W elements.
+ *   - Sampler state index i = 0..T: state 0 is the initial noise, state T the output.
+ */
+#ifndef PARAANYA_H
+#define PARAANYA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define PA_API __attribute__((visibility("default")))
+#else
+#define PA_API
+#endif
+
+/* ------------------------------------------------------------------ status codes */
+#define PA_OK               0
+#define PA_ERR_INVALID_ARG (-1)  /* argument outside the documented domain; nothing enqueued */
+#define PA_ERR_HIP         (-2)  /* a HIP runtime call failed (message names the call) */
+#define PA_ERR_OOM         (-3)  /* device or pinned-host allocation failed */
+#define PA_ERR_STATE       (-4)  /* call not valid in the handle's current state */
+#define PA_ERR_NONFINITE   (-5)  /* a residual of Eq. (2) was NaN/Inf; the sweep completed */
+#define PA_ERR_UNSUPPORTED (-6)  /* valid request this build does not implement */
+
+#define PA_MAX_WINDOW 256        /* largest window P */
+
+/* ------------------------------------------------------------------ schedule */
+#define PA_SCHED_SCALED_LINEAR 0
+#define PA_SCHED_EXPLICIT      1
+#define PA_SPACING_TRAILING    0
+
+/* Noise schedule of the DDIM sampler (the paper uses the SD-v1.5 DDIM scheduler,
+ * Sec. 3.3). SCALED_LINEAR: betas (sqrt(beta_start) + j*(sqrt(beta_end)-sqrt(beta_start))
+ * /(train_steps-1))^2, alpha_bar = cumprod(1-beta), trailing timesteps
+ * t_j = round(train_steps - j*train_steps/T) - 1, alpha_bar of the final state = 1
+ * (final_alpha_one must be 1). EXPLICIT: the caller gives alpha_bar[0..T] (host, state
+ * order, alpha_bar[T] is the clean end) and t_values[0..T-1] (host; used only for the
+ * time embedding of the patch-MLP). Copied at create. */
+typedef struct {
+    int32_t kind;
+    double beta_start, beta_end;
+    int32_t train_steps;
+    int32_t spacing;
+    int32_t final_alpha_one;
+    const double* alpha_bar;
+    const int32_t* t_values;
+} pa_schedule_t;
+
+/* ------------------------------------------------------------------ noise network */
+#define PA_EPS_LINEAR    0
+#define PA_EPS_PATCH_MLP 1
+
+/* Synthetic noise-prediction network standing in for the paper's SD-v1.5 UNet (Sec. 3.2).
+ * LINEAR: eps_j(x) = c[j] * x with c[0..T-1] (host fp32), j the sampling step.
+ * PATCH_MLP: 2x2 patchify (token = (h/2)*(W/2) + w/2, feature = c*4 + (h%2)*2 + (w%2),
+ * C = 4 channels, 16 features), h1 = GELU(bf16(x) W1 + e_j), h2 = GELU(bf16(h1) W2),
+ * eps = bf16(h2) W3, unpatchify; e_j = temb(t_j) Wt with the 128-d sinusoidal embedding
+ * (sin for k < 64, cos above, frequency exp(-ln(1e4) k/64)); erf GELU; bf16 x bf16
+ * products accumulated in fp32. Weights are bf16 bit patterns, row-major [in][out]:
+ * w1[16][hidden], wt[temb_dim][hidden], w2[hidden][hidden], w3[hidden][16]; host memory,
+ * copied at create. Supported: patch = 2, C = 4, temb_dim = 128, hidden in {512, 1024},
+ * (H/2)*(W/2) a multiple of 64. */
+typedef struct {
+    int32_t kind;
+    const float* c;
+    int32_t patch;
+    int32_t hidden;
+    int32_t temb_dim;
+    const uint16_t* w1;
+    const uint16_t* wt;
+    const uint16_t* w2;
+    const uint16_t* w3;
+} pa_eps_model_t;
+
+/* ------------------------------------------------------------------ create flags */
+#define PA_FLAG_TRACE   1u   /* keep a per-sweep trace record (paraanya_trace) */
+#define PA_FLAG_PROFILE 2u   /* time every network launch with HIP events (paraanya_kernel_times) */
+
+typedef struct paraanya paraanya_t;
+
+/* Counters of Sec. 3.1 / Tab. cache_tol: nfe = single-latent network evaluations (the
+ * misses), hits = window slots served from the cache, sweeps = Picard iterations. */
+typedef struct {
+    int64_t nfe;
+    int64_t hits;
+    int64_t misses;       /* == nfe */
+    int64_t sweeps;
+    int32_t window_start; /* s: states 0..s are final */
+    int32_t window_end;   /* e = min(s + P, T) */
+    int32_t done;         /* s >= T */
+    int32_t nonfinite;    /* a non-finite residual was seen (sticky until reset) */
+} pa_stats_t;
+
+/* One sweep's decisions (test hook). Slot j <-> timestep s + j, j < e - s. */
+typedef struct {
+    int32_t s, e, m, c, s_next, sweep;
+    double  dev[PA_MAX_WINDOW];       /* Eq. (4) per slot (fp64 sum); NaN for a first entry */
+    double  resid[PA_MAX_WINDOW];     /* Eq. (2) residual of state s + 1 + j (fp64 sum) */
+    int32_t miss_idx[PA_MAX_WINDOW];  /* ascending timesteps of the misses, m of them */
+    uint8_t hit[PA_MAX_WINDOW];       /* Eq. (5) hit mask per slot */
+} pa_sweep_trace_t;
+
+/* Device time of the network launches since reset (PA_FLAG_PROFILE). */
+typedef struct {
+    int64_t launches;
+    double  eps_ms_total;   /* summed kernel durations of the network launches */
+    int64_t eps_latents;    /* latents evaluated by those launches (= nfe) */
+} pa_ktimes_t;
+
+/* ------------------------------------------------------------------ entry points */
+
+/* Create a sampler. latent_shape = {N, C, H, W} with N = 1; T >= 1 sampling steps;
+ * window P in [1, min(T, PA_MAX_WINDOW)]; delta >= 0 the cache tolerance of Eq. (5)
+ * (strict '<'; 0 disables hits; +inf allowed); tol >= 0 the tau of Eq. (2) (mean
+ * square, '<='). Both thresholds are compared against fp64 sums: states and network
+ * outputs are stored in fp32, and the drift, the Picard sum, the deviations and the
+ * residuals are computed in fp64 from them, then rounded once on store. stream is a hipStream_t (NULL = the null stream). On success *out
+ * holds the handle; on failure *out = NULL and nothing is left allocated.
+ * Errors: INVALID_ARG (N != 1, C*H*W % 4 != 0, T < 1, window outside range, delta or tol
+ * negative/NaN, bad schedule or model fields), UNSUPPORTED (model shape not built),
+ * OOM, HIP. */
+PA_API int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_t* schedule,
+                           int32_t window, double delta, double tol, const pa_eps_model_t* eps_model,
+                           void* stream, uint32_t flags, paraanya_t** out);
+
+/* Start a new sample: state 0 <- x_init (device, D fp32, read on the stream), every cache
+ * entry invalid, window [0, min(P, T)), counters zero. Asynchronous. */
+PA_API int paraanya_reset(paraanya_t* h, const float* x_init);
+
+/* Enqueue one sweep (steps (1)-(6) above). If done != NULL the stream is synchronized and
+ * *done receives the done flag. Errors: STATE (before reset, or the last synchronized
+ * state was already done), NONFINITE (only when done != NULL and a residual was NaN/Inf). */
+PA_API int paraanya_sweep(paraanya_t* h, int32_t* done);
+
+/* reset, sweeps until done, then x_out (device, D fp32) <- state T. Returns after x_out
+ * is written (the stream is synchronized). x_init and x_out may alias. */
+PA_API int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out);
+
+/* Counters and window position; synchronizes the stream. STATE before the first reset. */
+PA_API int paraanya_stats(paraanya_t* h, pa_stats_t* out);
+
+/* Trace record of sweep k (0-based) since reset; needs PA_FLAG_TRACE. Synchronizes.
+ * INVALID_ARG if k is not a completed sweep; STATE without the flag. */
+PA_API int paraanya_trace(paraanya_t* h, int32_t k, pa_sweep_trace_t* out);
+
+/* Test hook: copy state rows to host memory; synchronizes. Any pointer may be NULL.
+ * X receives states [t0, t1) (t1 <= T+1); Xh, Eh, valid receive cache rows [t0, min(t1, T)).
+ * States above the newest computed one are stale until the next sweep fills them. */
+PA_API int paraanya_read_state(paraanya_t* h, int32_t t0, int32_t t1, float* X, float* Xh,
+                        float* Eh, uint8_t* valid);
+
+/* Test hook: the fp64 DDIM coefficients the device uses, alpha[i] = a_i - 1 and b[i]
+ * (host arrays of T), with d_i = alpha_i x_i + b_i eps_i, a_i = sqrt(ab_{i+1}/ab_i),
+ * b_i = sqrt(1 - ab_{i+1}) - a_i sqrt(1 - ab_i); and, for the patch-MLP, the fp32
+ * time-embedding table e[T][hidden] (host, may be NULL). */
+PA_API int paraanya_coefficients(paraanya_t* h, double* alpha, double* b, float* temb);
+
+/* Network-launch timings since reset (PA_FLAG_PROFILE); synchronizes. STATE without it. */
+PA_API int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out);
+
+/* Free every resource of the handle (synchronizes its stream first). NULL-safe. */
+PA_API void paraanya_destroy(paraanya_t* h);
+
+/* Thread-local message of the last failing call on this thread ("" if none). */
+PA_API const char* paraanya_last_error(void);
+
+/* Static name of a status code. */
+PA_API const char* paraanya_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PARAANYA_H */

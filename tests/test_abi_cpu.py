@@ -1,0 +1,107 @@
+"""The C-ABI library on the CPU: it loads, exports every entry point the header declares,
+and rejects invalid arguments before making any HIP call (no GPU needed)."""
+import ctypes as C
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_36522_amd import binding as B
+from paper_2609_36522_amd import inputs
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "paraanya.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"PA_API\s+[\w\s\*]*?\b(paraanya_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.load_library()
+    names = _declared()
+    assert len(names) == 12
+    assert sorted(B.EXPORTED) == names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    assert B.status_str(0) == "PA_OK"
+    assert B.status_str(-1) == "PA_ERR_INVALID_ARG"
+    assert B.status_str(-6) == "PA_ERR_UNSUPPORTED"
+    assert B.status_str(-99) == "PA_ERR_UNKNOWN"
+
+
+def _create(shape=(1, 4, 8, 8), T=10, window=4, delta=0.05, tol=1e-3, kind=B.PA_EPS_LINEAR,
+            hidden=1024, patch=2, temb_dim=128, sched=None, flags=0, null_c=False):
+    lib = B.load_library()
+    sh = (C.c_int32 * 4)(*shape)
+    sc = sched or B.Schedule(B.PA_SCHED_SCALED_LINEAR, 0.00085, 0.012, 1000, 0, 1, None, None)
+    c = np.ones(max(T, 1), np.float32)
+    w = {k: np.zeros(1, np.uint16) for k in ("w1", "wt", "w2", "w3")}
+    em = B.EpsModel(kind, None if null_c else c.ctypes.data_as(C.POINTER(C.c_float)), patch,
+                    hidden, temb_dim, *(w[k].ctypes.data_as(C.POINTER(C.c_uint16))
+                                        for k in ("w1", "wt", "w2", "w3")))
+    h = C.c_void_p(1234)
+    rc = lib.paraanya_create(sh, T, C.byref(sc), window, delta, tol, C.byref(em), None, flags,
+                             C.byref(h))
+    return rc, h.value, lib.paraanya_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,frag", [
+    (dict(shape=(2, 4, 8, 8)), "batch"),
+    (dict(shape=(1, 3, 3, 3)), "multiple of 4"),
+    (dict(T=0, window=1), "T must"),
+    (dict(window=0), "window"),
+    (dict(window=11), "window"),
+    (dict(T=300, window=257), "window"),
+    (dict(delta=-0.1), "delta"),
+    (dict(delta=float("nan")), "delta"),
+    (dict(tol=-1.0), "tol"),
+    (dict(tol=float("nan")), "tol"),
+    (dict(flags=8), "flags"),
+    (dict(null_c=True), "c is NULL"),
+    (dict(kind=7), "kind"),
+    (dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 4, 7, 8)), "even"),
+    (dict(T=2000, window=4), "train_steps"),
+])
+def test_create_rejects_invalid_arguments(kw, frag):
+    rc, h, msg = _create(**kw)
+    assert rc == B.PA_ERR_INVALID_ARG, msg
+    assert h is None
+    assert frag in msg
+
+
+@pytest.mark.parametrize("kw", [
+    dict(kind=B.PA_EPS_PATCH_MLP, hidden=768),
+    dict(kind=B.PA_EPS_PATCH_MLP, patch=4),
+    dict(kind=B.PA_EPS_PATCH_MLP, temb_dim=64),
+    dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 4, 10, 10)),   # 25 tokens: not a multiple of 64
+    dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 3, 16, 16)),
+])
+def test_create_reports_unbuilt_shapes(kw):
+    rc, h, msg = _create(**kw)
+    assert rc == B.PA_ERR_UNSUPPORTED, msg
+    assert h is None
+
+
+def test_explicit_schedule_validation():
+    ab = np.array([0.5, 0.7, 1.5], np.float64)       # > 1: invalid
+    tv = np.array([10, 5], np.int32)
+    sc = B.Schedule(B.PA_SCHED_EXPLICIT, 0, 0, 0, 0, 0, ab.ctypes.data_as(C.POINTER(C.c_double)),
+                    tv.ctypes.data_as(C.POINTER(C.c_int32)))
+    rc, h, msg = _create(T=2, window=2, sched=sc)
+    assert rc == B.PA_ERR_INVALID_ARG and "alpha_bar[2]" in msg
+
+
+def test_null_handle_calls_fail_cleanly():
+    lib = B.load_library()
+    assert lib.paraanya_reset(None, None) == B.PA_ERR_INVALID_ARG
+    assert lib.paraanya_sweep(None, None) == B.PA_ERR_INVALID_ARG
+    assert lib.paraanya_sample(None, None, None) == B.PA_ERR_INVALID_ARG
+    st = B.Stats()
+    assert lib.paraanya_stats(None, C.byref(st)) == B.PA_ERR_INVALID_ARG
+    lib.paraanya_destroy(None)   # NULL-safe

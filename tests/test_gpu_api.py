@@ -1,0 +1,124 @@
+"""C-ABI behaviour on the device: sample() against sweep-by-sweep, determinism, the state
+machine, non-finite input, explicit schedules, and the uploaded coefficient tables."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import eps_models as em
+from oracle import schedule as sch
+from paper_2609_36522_amd import binding as B
+from paper_2609_36522_amd import inputs
+from paper_2609_36522_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _x(wl, seed=0):
+    return torch.from_numpy(inputs.x_init(wl.latent, seed).reshape(-1)).cuda()
+
+
+@pytest.mark.parametrize("wl", [W.TINY_LINEAR, W.SMALL_MLP], ids=["linear", "mlp"])
+def test_sample_equals_sweep_by_sweep_and_is_deterministic(wl, gpu_lib):
+    x = _x(wl)
+    with B.from_workload(wl, trace=True) as s:
+        out1 = s.sample(x).cpu().numpy()
+        st1 = s.stats()
+        tr1 = s.traces()
+        out2 = s.sample(x).cpu().numpy()
+        st2 = s.stats()
+        tr2 = s.traces()
+        s.reset(x)
+        while not s.sweep(sync=True):
+            pass
+        st3 = s.stats()
+        X, _, _, _ = s.read_state(wl.T, wl.T + 1)
+    assert np.array_equal(out1, out2) and np.array_equal(out1, X[0])
+    assert st1 == st2 == st3
+    for a, b in zip(tr1, tr2):
+        assert a["miss"] == b["miss"] and a["c"] == b["c"]
+        assert np.array_equal(a["dev"], b["dev"], equal_nan=True) and np.array_equal(a["r"], b["r"])
+
+
+def test_state_machine(gpu_lib):
+    wl = W.TINY_LINEAR
+    with B.from_workload(wl) as s:
+        with pytest.raises(B.PAError) as ei:
+            s.sweep()
+        assert ei.value.code == B.PA_ERR_STATE
+        with pytest.raises(B.PAError) as ei:
+            s.stats()
+        assert ei.value.code == B.PA_ERR_STATE
+        with pytest.raises(B.PAError) as ei:
+            s.trace(0)
+        assert ei.value.code == B.PA_ERR_STATE      # no trace flag
+        s.sample(_x(wl))
+        with pytest.raises(B.PAError) as ei:
+            s.sweep()
+        assert ei.value.code == B.PA_ERR_STATE      # already done
+        with pytest.raises(B.PAError) as ei:
+            s.kernel_times()
+        assert ei.value.code == B.PA_ERR_STATE
+    with B.from_workload(wl, trace=True) as s:
+        s.sample(_x(wl))
+        n = s.stats()["sweeps"]
+        with pytest.raises(B.PAError) as ei:
+            s.trace(n)
+        assert ei.value.code == B.PA_ERR_INVALID_ARG
+
+
+def test_nonfinite_input_is_reported(gpu_lib):
+    wl = W.TINY_LINEAR
+    x = _x(wl)
+    x[5] = float("nan")
+    with B.from_workload(wl) as s:
+        with pytest.raises(B.PAError) as ei:
+            s.sample(x)
+        assert ei.value.code == B.PA_ERR_NONFINITE
+        st = s.stats()
+        assert st["done"] and st["nonfinite"] and st["sweeps"] == wl.T   # stride 1 on NaN
+        out = s.sample(_x(wl))                  # the handle recovers after reset
+        assert np.isfinite(out.cpu().numpy()).all()
+
+
+def test_explicit_schedule_matches_scaled_linear(gpu_lib):
+    wl = W.TINY_LINEAR
+    ab, t = sch.sampler_alpha_bar(wl.T)
+    x = _x(wl)
+    with B.from_workload(wl) as s1, B.from_workload(wl, schedule={"alpha_bar": ab, "t_values": t}) as s2:
+        a1, b1, _ = s1.coefficients()
+        a2, b2, _ = s2.coefficients()
+        assert np.array_equal(a1, a2) and np.array_equal(b1, b2)
+        assert np.array_equal(s1.sample(x).cpu().numpy(), s2.sample(x).cpu().numpy())
+
+
+@pytest.mark.parametrize("T", [10, 50, 100, 1000])
+def test_uploaded_coefficients_are_rounded_oracle_values(T, gpu_lib):
+    wl = W.TINY_LINEAR.with_(T=T, window=min(4, T))
+    ab, t = sch.sampler_alpha_bar(T)
+    alpha, b = sch.ddim_coefficients(ab)
+    with B.from_workload(wl) as s:
+        a32, b32, _ = s.coefficients()
+    # Same fp64 definition on both sides: bit-identical coefficient tables.
+    assert np.array_equal(a32, alpha) and np.array_equal(b32, b)
+
+
+def test_time_embedding_table(gpu_lib):
+    wl = W.SMALL_MLP
+    ab, t = sch.sampler_alpha_bar(wl.T)
+    net = em.PatchMLP(inputs.mlp_weights(wl.hidden), t, wl.latent)
+    with B.from_workload(wl) as s:
+        _, _, temb = s.coefficients()
+    diff = np.abs(temb.astype(np.float64) - net.temb.astype(np.float64))
+    assert np.all(diff <= np.abs(net.temb) * 2.0 ** -23 + 1e-30)
+
+
+def test_profile_counts_launches(gpu_lib):
+    wl = W.SMALL_MLP
+    with B.from_workload(wl, profile=True) as s:
+        s.sample(_x(wl))
+        kt = s.kernel_times()
+        st = s.stats()
+    assert kt["launches"] == st["sweeps"] and kt["eps_latents"] == st["nfe"]
+    assert kt["eps_ms_total"] > 0

@@ -1,0 +1,90 @@
+"""Device parity against the oracle through the C ABI (MI355X only).
+
+Every case runs the device sampler sweep by sweep; the oracle repeats each sweep on the
+device's own pre-sweep state (step-locked) and then follows its own trajectory from the
+same initial latent. Decisions must agree except inside the 1e-6 relative band around
+delta/tau; final latents agree within 1e-4 x RMS.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2609_36522_amd import workloads as W
+from paper_2609_36522_amd.workloads import Workload
+
+import parity_harness as H
+
+pytestmark = pytest.mark.gpu
+
+INF = math.inf
+
+LIN = W.TINY_LINEAR
+CASES = [
+    # tiny closed-form workload and its degenerate settings
+    ("tiny", LIN, 0.05),
+    ("tiny_delta0", LIN, 0.0),
+    ("tiny_delta_inf", LIN, INF),
+    ("tiny_window1", LIN.with_(window=1), 0.05),
+    ("tiny_windowT", LIN.with_(window=10), 0.05),
+    ("T1", LIN.with_(T=1, window=1), 0.05),
+    ("tau0", LIN.with_(tol=0.0), 0.05),
+    # ragged sizes: partial cache-test chunks and Picard column blocks
+    ("ragged_4x10x10", Workload("lin_4x10x10", (4, 10, 10), 30, 7, 0.05, 1e-3, "linear"), 0.05),
+    ("ragged_3x5x4", Workload("lin_3x5x4", (3, 5, 4), 12, 5, 0.1, 1e-3, "linear"), 0.1),
+    ("D4", Workload("lin_1x2x2", (1, 2, 2), 8, 3, 0.05, 1e-3, "linear"), 0.05),
+    ("big_D_linear", Workload("lin_4x64x64", (4, 64, 64), 100, 32, 0.05, 1e-3, "linear"), 0.05),
+    # maximum window
+    ("max_window", Workload("lin_4x8x8_P256", (4, 8, 8), 256, 256, 0.05, 1e-3, "linear"), 0.05),
+    ("long_window_128", Workload("lin_4x16x16_P128", (4, 16, 16), 300, 128, 0.05, 1e-3, "linear"), 0.05),
+    # patch-MLP
+    ("mlp_16x32_H512", Workload("mlp_4x16x32_H512", (4, 16, 32), 20, 8, 0.05, 1e-3, "patch_mlp",
+                                hidden=512), 0.05),
+    ("mlp_small", W.SMALL_MLP, 0.05),
+    ("mlp_small_delta0", W.SMALL_MLP, 0.0),
+    ("mlp_sd", W.SD_MLP, 0.05),
+    ("mlp_sd_delta0", W.SD_MLP, 0.0),
+]
+
+
+@pytest.mark.parametrize("name,wl,delta", CASES, ids=[c[0] for c in CASES])
+def test_parity(name, wl, delta, gpu_lib):
+    print(f"[parity] {name}: {wl.name} delta={delta}", flush=True)
+    run = H.Run(wl, delta, verify_eps=6).run()
+    try:
+        st = run.stats
+        assert st["done"] and st["sweeps"] == len(run.records) <= wl.T
+        assert st["nfe"] >= wl.T and st["nfe"] == sum(r["m"] for r in run.records)
+        assert st["hits"] == sum(r["e"] - r["s"] - r["m"] for r in run.records)
+        if delta == 0.0:
+            assert st["hits"] == 0
+        if delta == INF:
+            assert st["nfe"] == wl.T
+        if wl.window == 1:
+            assert st["sweeps"] == wl.T and st["nfe"] == wl.T
+        assert run.records[0]["m"] == min(wl.window, wl.T)
+        err = run.follow()
+        assert err <= H.FINAL_RTOL, f"final latent off by {err:.3g} x RMS"
+        print(f"[parity] {name}: sweeps={st['sweeps']} nfe={st['nfe']} hits={st['hits']} "
+              f"final_err={err:.2e} eps_err_max={max(run.eps_err, default=0):.2e} "
+              f"state_ulp_diffs={run.state_diffs} "
+              f"flips={len(run.log.flips) + len(run.follow_log.flips)}", flush=True)
+    finally:
+        run.close()
+
+
+def test_long_window_sd(gpu_lib):
+    """Full-size long-window workload (T=1000, window 128): every sweep step-locked, sampled
+    network outputs checked one by one, eps-locked follow to the final latent."""
+    wl = W.LONG_MLP
+    print(f"[parity] long: {wl.name}", flush=True)
+    run = H.Run(wl, 0.05, verify_eps=10).run()
+    try:
+        err = run.follow()
+        assert err <= H.FINAL_RTOL
+        assert run.stats["nfe"] >= wl.T
+        print(f"[parity] long: sweeps={run.stats['sweeps']} nfe={run.stats['nfe']} "
+              f"hits={run.stats['hits']} final_err={err:.2e}", flush=True)
+    finally:
+        run.close()
