@@ -86,7 +86,7 @@ typedef struct {
  * products accumulated in fp32. Weights are bf16 bit patterns, row-major [in][out]:
  * w1[16][hidden], wt[temb_dim][hidden], w2[hidden][hidden], w3[hidden][16]; host memory,
  * copied at create. Supported: patch = 2, C = 4, temb_dim = 128, hidden in {512, 1024},
- * (H/2)*(W/2) a multiple of 64. */
+ * (H/2)*(W/2) a multiple of 128. */
 typedef struct {
     int32_t kind;
     const float* c;
@@ -172,7 +172,8 @@ PA_API int paraanya_trace(paraanya_t* h, int32_t k, pa_sweep_trace_t* out);
 
 /* Test hook: copy state rows to host memory; synchronizes. Any pointer may be NULL.
  * X receives states [t0, t1) (t1 <= T+1); Xh, Eh, valid receive cache rows [t0, min(t1, T)).
- * States above the newest computed one are stale until the next sweep fills them. */
+ * A state above the newest computed one is not materialized: its current estimate is the
+ * newest computed state (the window start's row shows which rows were computed). */
 PA_API int paraanya_read_state(paraanya_t* h, int32_t t0, int32_t t1, float* X, float* Xh,
                         float* Eh, uint8_t* valid);
 

@@ -1,15 +1,22 @@
 // Batched evaluation of the cache misses by the patch-MLP noise network, one fused
-// persistent kernel for gfx950 (the "single batched forward pass" over the misses, Sec. 2.2).
+// persistent kernel for gfx950 (the single batched forward pass over the misses, Sec. 2.2).
 //
-// Work item = (miss j, block of 64 tokens). For one item the block
-//   0. gathers the 64 tokens (2x2 patches, 16 features) of latent x_t, rounds to bf16;
-//   1. h1^T = GELU(W1^T x^T + e_t)     : MFMA 32x32x16 bf16, K = 16; bf16 result kept in LDS;
-//   2. h2^T = GELU(W2^T h1^T)          : MFMA 32x32x16 bf16, K = hidden; each wave owns 128
-//                                        output units and streams its W2^T rows from L2;
-//   3. eps^T = W3^T h2^T               : MFMA again, fed straight from the GEMM2 accumulators
-//                                        (the reduction index is permuted to match the
-//                                        accumulator layout; W3 is stored pre-permuted);
-//   4. sums the per-wave partials in a fixed order, unpatchifies and writes Eh[t].
+// Work item = (miss j, block of 128 tokens, half of the hidden-out units of GEMM2). For one
+// item the block
+//   0. gathers the 128 tokens (2x2 patches, 16 features) of latent x_t, rounds to bf16;
+//   1. h1^T = GELU(W1^T x^T + e_t) in K-chunks of 256 units: MFMA 32x32x16 bf16, K = 16; bf16
+//      result in LDS ([token][unit], padded rows), two chunk buffers of 66 KB;
+//   2. h2^T += W2^T h1^T chunk by chunk: each of the 8 waves owns 64 output units x 128
+//      tokens (128 accumulator registers); W2^T fragments stream from L2 in MFMA-fragment
+//      order (1 KB contiguous per wave load), two register stages in flight; the GEMM1 and
+//      GELU of chunk c + 1 are computed between the MFMA groups of chunk c;
+//   3. eps^T = W3^T GELU(h2^T), MFMA fed straight from the GEMM2 accumulators (reduction
+//      index permuted to the accumulator layout; W3 stored pre-permuted);
+//   4. per-wave partials summed in a fixed order through LDS, unpatchified, written as this
+//      half's partial output; the Picard kernel adds the halves in a fixed order and writes
+//      the cache.
+// 128 tokens per item make every W2 byte feed 128 FLOP, which keeps the W2 stream under the
+// per-CU vector-memory bandwidth; the price is computing h1 once per half.
 // All products are bf16 x bf16 with fp32 accumulation.
 //
 // Accumulator layout of v_mfma_f32_32x32x16_bf16 (C/D, 16 floats per lane):
@@ -18,7 +25,7 @@
 // use the same lane->slot convention, so any consistent slot->k assignment is valid.
 #include <math.h>
 
-#include "pa_internal.h"
+#include "pa_device.h"
 
 namespace pa {
 
@@ -28,31 +35,33 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kTok = 64;                // tokens per work item
+constexpr int kTok = 128;               // tokens per work item
+constexpr int kNH = 512;                // GEMM2 output units per work item
+constexpr int kKC = 256;                // h1 units per LDS buffer (K-chunk); two buffers
+constexpr int kWaves = 8;               // wave w owns output units [64w, 64w + 64) of the item
 constexpr int kFeat = 16;               // 2x2 patch x 4 channels
 constexpr int kXRow = kFeat + 8;        // padded LDS row of the token tile (bf16)
 
-// erf-GELU, x * Phi(x), branch-free. The normal upper tail Q(a) = 1 - Phi(a), a = |x|, is
-// Hastings' approximation (Abramowitz & Stegun 26.2.17): Q(a) = phi(a) t (b1 + t (b2 + ...)),
-// t = 1 / (1 + p a), |error| < 7.5e-8; phi(a) = exp(-a^2/2) / sqrt(2 pi) is folded into the
-// coefficients. Error of the result <= ~2.2e-7 |x| in fp32, far below the bf16 rounding that
-// follows. One v_rcp_f32 and one v_exp_f32 per element.
+// erf-GELU, x * Phi(x) = max(x, 0) - a Q(a) with a = |x| and Q the normal upper tail,
+// branch-free. Q(a) = 2^(-P(min(a, 5.5))) with P a degree-10 polynomial fitted toward the
+// minimax relative error of Q (derivation: gelu_fit.py). One v_exp_f32 and eleven FMA-class
+// instructions per element; in fp32 the result is within 1.4e-7 max(1, |x|) of the exact
+// erf GELU and within 3e-7 (x > 0) / 1.5e-6 (x < 0) relative, well below the bf16 rounding
+// that follows.
 __device__ __forceinline__ float gelu_erf(float x) {
-    constexpr float kP = 0.2316419f;
-    constexpr float kB1 = 0.319381530f * 0.39894228040143268f;
-    constexpr float kB2 = -0.356563782f * 0.39894228040143268f;
-    constexpr float kB3 = 1.781477937f * 0.39894228040143268f;
-    constexpr float kB4 = -1.821255978f * 0.39894228040143268f;
-    constexpr float kB5 = 1.330274429f * 0.39894228040143268f;
-    constexpr float kHalfLog2e = -0.72134752044448170f;   // -log2(e) / 2
-    const float a = fabsf(x);
-    const float t = __builtin_amdgcn_rcpf(fmaf(kP, a, 1.0f));
-    float poly = fmaf(t, kB5, kB4);
-    poly = fmaf(t, poly, kB3);
-    poly = fmaf(t, poly, kB2);
-    poly = fmaf(t, poly, kB1);
-    const float q = __builtin_amdgcn_exp2f(a * (a * kHalfLog2e)) * (poly * t);
-    return x * (x >= 0.0f ? 1.0f - q : q);
+    const float a = fminf(fabsf(x), 5.5f);
+    float p = fmaf(a, 1.7772681104588628e-08f, -5.619335752271581e-07f);
+    p = fmaf(p, a, 7.6224991971685085e-06f);
+    p = fmaf(p, a, -5.5895987316034734e-05f);
+    p = fmaf(p, a, 0.00020456546917557716f);
+    p = fmaf(p, a, 0.00016647430311422795f);
+    p = fmaf(p, a, -0.007166667375713587f);
+    p = fmaf(p, a, 0.05260409414768219f);
+    p = fmaf(p, a, 0.4591609537601471f);
+    p = fmaf(p, a, 1.1511125564575195f);
+    p = fmaf(p, a, 0.9999998211860657f);
+    const float q = __builtin_amdgcn_exp2f(-p);
+    return fmaf(-fabsf(x), q, fmaxf(x, 0.0f));
 }
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -65,7 +74,7 @@ struct TokPos {
     int tl, f, idx;
 };
 __device__ __forceinline__ TokPos tok_pos(int e, int tb, int Himg, int Wimg) {
-    const int dw = e & 1, tl = (e >> 1) & 63, dh = (e >> 7) & 1, c = e >> 8;
+    const int dw = e & 1, tl = (e >> 1) & (kTok - 1), dh = (e >> 8) & 1, c = e >> 9;
     const int half_w = Wimg >> 1;
     const int tok = tb * kTok + tl;
     const int hp = tok / half_w, wp = tok - hp * half_w;
@@ -79,28 +88,41 @@ __device__ __forceinline__ TokPos tok_pos(int e, int tb, int Himg, int Wimg) {
 }  // namespace
 
 template <int H>
-__global__ __launch_bounds__(H / 2) void k_eps_mlp(Dev d) {
-    constexpr int NW = H / 128;          // waves; wave w owns hidden units [128w, 128w+128)
-    constexpr int NT = NW * 64;
-    constexpr int HRow = H + 8;          // padded LDS row of h1 (bf16)
-    constexpr int KB = H / 32;           // GEMM2 k-blocks of 32
-    __shared__ __attribute__((aligned(16))) __bf16 h1s[kTok * HRow];
+__global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
+    constexpr int NT = kWaves * 64;
+    constexpr int NS = H / kNH;          // halves of the output units (work items per tokens)
+    constexpr int KCH = H / kKC;         // K-chunks of h1
+    constexpr int HRow = kKC + 8;        // padded LDS row of h1 (bf16)
+    constexpr int KS = H / 16;           // GEMM2 k-steps (fragment columns of W2^T)
+    constexpr int KBC = kKC / 32;        // k-blocks (two k-steps) per chunk
+    constexpr int ITER = KBC / 2;        // pipelined iterations per chunk
+    static_assert(H % kNH == 0 && H % kKC == 0 && ITER == 4, "unsupported hidden width");
+    static_assert(kKC == kWaves * 32, "each wave computes 32 h1 units of a chunk");
+    // h1 chunks, double-buffered: chunk c + 1 is computed while GEMM2 consumes chunk c.
+    __shared__ __attribute__((aligned(16))) __bf16 h1s[2][kTok * HRow];
     __shared__ __attribute__((aligned(16))) __bf16 xs[kTok * kXRow];
-    float* red = reinterpret_cast<float*>(h1s);   // [NW][kTok][16] after GEMM2
+    float* red = reinterpret_cast<float*>(&h1s[0][0]);   // [kWaves][kTok][16] after GEMM2
+    static_assert(kWaves * kTok * kFeat * 4 <= 2 * kTok * HRow * 2, "reduction buffer must fit");
 
     const Ctrl* ctrl = d.ctrl;
     if (ctrl->done) return;
     const int nblk = d.ntok / kTok;
-    const int items = ctrl->m * nblk;
+    const int items = ctrl->m * nblk * NS;
+    const int newest = ctrl->newest;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int g = lane >> 5, l32 = lane & 31;
     const f32x16 zero16 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
                            0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const bf16x8* w2lane = reinterpret_cast<const bf16x8*>(d.w2f) + lane;
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        const int jm = item / nblk, tb = item - jm * nblk;
+        const int ns = item % NS;
+        const int rest = item / NS;
+        const int tb = rest % nblk, jm = rest / nblk;
         const int t = ctrl->miss_idx[jm];
-        const float* xt = d.X + (size_t)t * d.D;
+        const float* xt = d.X + (size_t)min(t, newest) * d.D;   // states beyond newest: its copy
+        const float* et = d.temb + (size_t)t * H;
+        const int hb0 = ns * (kNH / 32) + w * 2;   // this wave's first 32-unit block of W2^T
 
         // ---- 0. gather + patchify + bf16
         for (int e = tid; e < kTok * kFeat; e += NT) {
@@ -109,111 +131,131 @@ __global__ __launch_bounds__(H / 2) void k_eps_mlp(Dev d) {
         }
         __syncthreads();
 
-        // ---- 1. h1 = GELU(x W1 + e_t) -> bf16 in LDS, row = token
-        {
-            const float* et = d.temb + (size_t)t * H;
+        // ---- 1. h1 = GELU(x W1 + e_t): wave w computes units [32w, 32w + 32) of a chunk,
+        // one 32-token slice per call, into LDS rows [token][unit].
+        bf16x8 w1a;
+        const float* ek = et;                // e_t of the chunk's units (read where used)
+        auto h1_setup = [&](int kc) {
+            const int n0 = kc * kKC + w * 32;
+            w1a = *reinterpret_cast<const bf16x8*>(d.w1t + (size_t)(n0 + l32) * kFeat + g * 8);
+            ek = et + n0 + g * 4;
+        };
+        f32x16 h1acc;
+        auto h1_mfma = [&](int tb4) {
+            const bf16x8 b = *reinterpret_cast<const bf16x8*>(xs + (tb4 * 32 + l32) * kXRow + g * 8);
+            h1acc = mfma32(w1a, b, zero16);
+        };
+        auto h1_gelu = [&](__bf16* buf, int tb4, int q0) {   // units q0*8.. of the slice
+            const int tok = tb4 * 32 + l32;
 #pragma unroll
-            for (int hb = 0; hb < 4; ++hb) {
-                const int n0 = w * 128 + hb * 32;
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(d.w1t + (size_t)(n0 + l32) * kFeat + g * 8);
-                float4 ev[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) ev[q] = *reinterpret_cast<const float4*>(et + n0 + q * 8 + g * 4);
-#pragma unroll
-                for (int tb2 = 0; tb2 < 2; ++tb2) {
-                    const int tok = tb2 * 32 + l32;
-                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(xs + tok * kXRow + g * 8);
-                    const f32x16 acc = mfma32(a, b, zero16);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        bf16x4 v;
-                        v[0] = (__bf16)gelu_erf(acc[q * 4 + 0] + ev[q].x);
-                        v[1] = (__bf16)gelu_erf(acc[q * 4 + 1] + ev[q].y);
-                        v[2] = (__bf16)gelu_erf(acc[q * 4 + 2] + ev[q].z);
-                        v[3] = (__bf16)gelu_erf(acc[q * 4 + 3] + ev[q].w);
-                        *reinterpret_cast<bf16x4*>(h1s + tok * HRow + n0 + q * 8 + g * 4) = v;
-                    }
-                }
+            for (int q = q0; q < q0 + 2; ++q) {
+                const float4 ev = *reinterpret_cast<const float4*>(ek + q * 8);
+                bf16x4 v;
+                v[0] = (__bf16)gelu_erf(h1acc[q * 4 + 0] + ev.x);
+                v[1] = (__bf16)gelu_erf(h1acc[q * 4 + 1] + ev.y);
+                v[2] = (__bf16)gelu_erf(h1acc[q * 4 + 2] + ev.z);
+                v[3] = (__bf16)gelu_erf(h1acc[q * 4 + 3] + ev.w);
+                *reinterpret_cast<bf16x4*>(buf + tok * HRow + w * 32 + q * 8 + g * 4) = v;
             }
-        }
+        };
+        auto h1_slice = [&](__bf16* buf, int tb4) {
+            h1_mfma(tb4);
+            h1_gelu(buf, tb4, 0);
+            h1_gelu(buf, tb4, 2);
+        };
+        h1_setup(0);
+#pragma unroll
+        for (int tb4 = 0; tb4 < 4; ++tb4) h1_slice(h1s[0], tb4);
         __syncthreads();
 
-        // ---- 2. h2^T = W2^T h1^T, k-block of 32: lane group g takes k = 32kb + 16g + [0,16)
-        f32x16 acc2[4][2];
+        f32x16 acc2[2][4];
 #pragma unroll
-        for (int hb = 0; hb < 4; ++hb)
+        for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
-            for (int tb2 = 0; tb2 < 2; ++tb2) acc2[hb][tb2] = zero16;
-        const __bf16* wrow = d.w2t + (size_t)(w * 128 + l32) * H + g * 16;
-        bf16x8 A[4][2];
+            for (int tb4 = 0; tb4 < 4; ++tb4) acc2[hb][tb4] = zero16;
+
+        for (int kc = 0; kc < KCH; ++kc) {
+            // ---- 2. acc2 += W2^T h1^T over chunk kc (two register stages of W2^T fragments),
+            // with chunk kc + 1's h1 slices computed in between (the other wave of the SIMD
+            // can issue VALU while this one waits on the matrix core).
+            const bool more = kc + 1 < KCH;
+            if (more) h1_setup(kc + 1);
+            __bf16* nbuf = h1s[(kc + 1) & 1];
+            const bf16x8* wa = w2lane + ((size_t)hb0 * KS + kc * (kKC / 16)) * 64;
+            const __bf16* h1b = h1s[kc & 1] + l32 * HRow + g * 8;
+            bf16x8 A0[2][2], A1[2][2];
+            auto load_a = [&](bf16x8 (&A)[2][2], int kb) {
 #pragma unroll
-        for (int hb = 0; hb < 4; ++hb)
+                for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                A[hb][j] = *reinterpret_cast<const bf16x8*>(wrow + (size_t)hb * 32 * H + j * 8);
-        for (int kb = 0; kb < KB; ++kb) {
-            bf16x8 An[4][2];
-            const int kn = (kb + 1 < KB) ? kb + 1 : kb;
+                    for (int j = 0; j < 2; ++j) A[hb][j] = wa[((size_t)hb * KS + 2 * kb + j) * 64];
+            };
+            auto mma = [&](const bf16x8 (&A)[2][2], int kb) {
 #pragma unroll
-            for (int hb = 0; hb < 4; ++hb)
+                for (int tb4 = 0; tb4 < 4; ++tb4) {
+                    bf16x8 B[2];
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    An[hb][j] = *reinterpret_cast<const bf16x8*>(wrow + (size_t)hb * 32 * H + kn * 32 + j * 8);
-            bf16x8 B[2][2];
+                    for (int j = 0; j < 2; ++j)
+                        B[j] = *reinterpret_cast<const bf16x8*>(h1b + tb4 * 32 * HRow + kb * 32 + j * 16);
 #pragma unroll
-            for (int tb2 = 0; tb2 < 2; ++tb2)
+                    for (int j = 0; j < 2; ++j)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    B[tb2][j] = *reinterpret_cast<const bf16x8*>(h1s + (tb2 * 32 + l32) * HRow + kb * 32 + g * 16 + j * 8);
+                        for (int hb = 0; hb < 2; ++hb)
+                            acc2[hb][tb4] = mfma32(A[hb][j], B[j], acc2[hb][tb4]);
+                }
+            };
+            load_a(A0, 0);
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-#pragma unroll
-                for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-                    for (int tb2 = 0; tb2 < 2; ++tb2)
-                        acc2[hb][tb2] = mfma32(A[hb][j], B[tb2][j], acc2[hb][tb2]);
-#pragma unroll
-            for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-                for (int j = 0; j < 2; ++j) A[hb][j] = An[hb][j];
+            for (int it = 0; it < ITER; ++it) {
+                const int kb = 2 * it;
+                load_a(A1, kb + 1);
+                __builtin_amdgcn_sched_barrier(0);
+                mma(A0, kb);
+                if (more) h1_slice(nbuf, it);
+                __builtin_amdgcn_sched_barrier(0);
+                load_a(A0, kb + 2 < KBC ? kb + 2 : KBC - 1);
+                __builtin_amdgcn_sched_barrier(0);
+                mma(A1, kb + 1);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __syncthreads();                 // chunk kc + 1 complete; chunk kc's buffer free
         }
 
-        // ---- 3. eps^T += W3p h2^T straight from the accumulators (slot jj*8+i <-> reg jj*8+i)
-        f32x16 acc3[2] = {zero16, zero16};
+        // ---- 3. eps^T partial = W3p GELU(h2^T) straight from the accumulators
+        f32x16 acc3[4] = {zero16, zero16, zero16, zero16};
 #pragma unroll
-        for (int hb = 0; hb < 4; ++hb) {
+        for (int hb = 0; hb < 2; ++hb) {
 #pragma unroll
             for (int jj = 0; jj < 2; ++jj) {
                 const bf16x8 a3 = *reinterpret_cast<const bf16x8*>(
-                    d.w3p + (((size_t)(w * 4 + hb) * 2 + jj) * 64 + lane) * 8);
+                    d.w3p + (((size_t)(hb0 + hb) * 2 + jj) * 64 + lane) * 8);
 #pragma unroll
-                for (int tb2 = 0; tb2 < 2; ++tb2) {
+                for (int tb4 = 0; tb4 < 4; ++tb4) {
                     bf16x8 b3;
 #pragma unroll
-                    for (int i = 0; i < 8; ++i) b3[i] = (__bf16)gelu_erf(acc2[hb][tb2][jj * 8 + i]);
-                    acc3[tb2] = mfma32(a3, b3, acc3[tb2]);
+                    for (int i = 0; i < 8; ++i) b3[i] = (__bf16)gelu_erf(acc2[hb][tb4][jj * 8 + i]);
+                    acc3[tb4] = mfma32(a3, b3, acc3[tb4]);
                 }
             }
         }
-        __syncthreads();                 // every wave is done reading h1s
-        // valid rows of acc3: regs 0..7 -> feature (r/4)*8 + g*4 + r%4, token tb2*32 + l32
+        // valid rows of acc3: regs 0..7 -> feature (r/4)*8 + g*4 + r%4, token tb4*32 + l32
 #pragma unroll
-        for (int tb2 = 0; tb2 < 2; ++tb2) {
-            float* dst = red + ((size_t)w * kTok + tb2 * 32 + l32) * kFeat;
+        for (int tb4 = 0; tb4 < 4; ++tb4) {
+            float* dst = red + ((size_t)w * kTok + tb4 * 32 + l32) * kFeat;
             *reinterpret_cast<float4*>(dst + g * 4) =
-                make_float4(acc3[tb2][0], acc3[tb2][1], acc3[tb2][2], acc3[tb2][3]);
+                make_float4(acc3[tb4][0], acc3[tb4][1], acc3[tb4][2], acc3[tb4][3]);
             *reinterpret_cast<float4*>(dst + 8 + g * 4) =
-                make_float4(acc3[tb2][4], acc3[tb2][5], acc3[tb2][6], acc3[tb2][7]);
+                make_float4(acc3[tb4][4], acc3[tb4][5], acc3[tb4][6], acc3[tb4][7]);
         }
         __syncthreads();
 
-        // ---- 4. fixed-order sum over waves, unpatchify, store the fresh output
-        float* out = d.Eh + (size_t)t * d.D;
+        // ---- 4. fixed-order sum over waves, unpatchify, store this half's partial output
+        float* out = d.Ep + ((size_t)ns * d.P + jm) * d.D;
         for (int e = tid; e < kTok * kFeat; e += NT) {
             const TokPos p = tok_pos(e, tb, d.Himg, d.Wimg);
             float sum = 0.f;
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) sum += red[((size_t)ww * kTok + p.tl) * kFeat + p.f];
+            for (int ww = 0; ww < kWaves; ++ww) sum += red[((size_t)ww * kTok + p.tl) * kFeat + p.f];
             out[p.idx] = sum;
         }
         __syncthreads();                 // LDS is reused by the next item
@@ -222,15 +264,19 @@ __global__ __launch_bounds__(H / 2) void k_eps_mlp(Dev d) {
 
 int mlp_supported(int hidden) { return hidden == 512 || hidden == 1024; }
 
+int mlp_tokens_per_item() { return kTok; }
+
+int mlp_splits(int hidden) { return hidden / kNH; }
+
 int mlp_grid_size(int device_cus) { return device_cus > 0 ? device_cus : 256; }
 
 hipError_t launch_eps_mlp(const Dev& d, hipStream_t st) {
     switch (d.hidden) {
         case 512:
-            hipLaunchKernelGGL(k_eps_mlp<512>, dim3(d.mlp_grid), dim3(256), 0, st, d);
+            hipLaunchKernelGGL(k_eps_mlp<512>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, d);
             break;
         case 1024:
-            hipLaunchKernelGGL(k_eps_mlp<1024>, dim3(d.mlp_grid), dim3(512), 0, st, d);
+            hipLaunchKernelGGL(k_eps_mlp<1024>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, d);
             break;
         default:
             return hipErrorInvalidValue;

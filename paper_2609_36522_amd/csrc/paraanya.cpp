@@ -112,7 +112,7 @@ struct paraanya {
     }
 
     int enqueue_sweep() {
-        PA_HIP(pa::launch_cache_test(d, stream));
+        // The miss list of this sweep was published by the previous k_slide (or k_reset).
         if (model == PA_EPS_PATCH_MLP) {
             hipEvent_t e0 = nullptr, e1 = nullptr;
             if (flags & PA_FLAG_PROFILE) {
@@ -126,6 +126,7 @@ struct paraanya {
             if (flags & PA_FLAG_PROFILE) PA_HIP(hipEventRecord(e1, stream));
         }
         PA_HIP(pa::launch_picard(d, stream, model == PA_EPS_LINEAR));
+        PA_HIP(pa::launch_slide(d, stream));
         return PA_OK;
     }
 };
@@ -221,7 +222,8 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
         if (Hi % 2 || Wi % 2) return fail(PA_ERR_INVALID_ARG, "patch-MLP: H and W must be even");
         if (em->temb_dim != 128) return fail(PA_ERR_UNSUPPORTED, "patch-MLP: only temb_dim = 128 is built");
         if (!pa::mlp_supported(em->hidden)) return fail(PA_ERR_UNSUPPORTED, "patch-MLP: hidden %d not built (512, 1024)", em->hidden);
-        if (((Hi / 2) * (Wi / 2)) % 64) return fail(PA_ERR_UNSUPPORTED, "patch-MLP: token count must be a multiple of 64");
+        if (((Hi / 2) * (Wi / 2)) % pa::mlp_tokens_per_item())
+            return fail(PA_ERR_UNSUPPORTED, "patch-MLP: token count must be a multiple of %d", pa::mlp_tokens_per_item());
     } else {
         return fail(PA_ERR_INVALID_ARG, "unknown eps model kind %d", em->kind);
     }
@@ -249,7 +251,6 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     Dev& d = h->d;
     d.T = T; d.P = window; d.D = D; d.C = C; d.Himg = Hi; d.Wimg = Wi;
     d.delta = delta; d.tol = tol;
-    d.test_chunks = pa::cache_test_chunks(D);
     d.picard_blocks = pa::picard_blocks(D);
     auto bail = [&](int code) { delete h; return code; };
 
@@ -266,8 +267,8 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     if ((rc = h->alloc(&d.Eh, (size_t)T * Dz, "Eh"))) return bail(rc);
     if ((rc = h->alloc(&d.valid, (size_t)T, "valid"))) return bail(rc);
     if ((rc = h->alloc(&d.coef, 2 * (size_t)T, "coef"))) return bail(rc);
-    if ((rc = h->alloc(&d.part_test, (size_t)(window + 1) * d.test_chunks, "part_test"))) return bail(rc);
     if ((rc = h->alloc(&d.part_res, (size_t)window * d.picard_blocks, "part_res"))) return bail(rc);
+    if ((rc = h->alloc(&d.part_dev, (size_t)window * d.picard_blocks, "part_dev"))) return bail(rc);
     if ((rc = h->alloc(&d.ctrl, 1, "ctrl"))) return bail(rc);
     if (flags & PA_FLAG_TRACE)
         if ((rc = h->alloc(&d.trace, (size_t)T, "trace"))) return bail(rc);
@@ -292,13 +293,20 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
         d.ntok = (Hi / 2) * (Wi / 2);
         d.mlp_grid = pa::mlp_grid_size(cus);
         h->temb_dim = em->temb_dim;
-        // Device layouts: W1^T [H][16], W2^T [H][H] (row = output unit), W3 fragments
-        // permuted to the GEMM2 accumulator layout (see k_epsnet.hip).
-        std::vector<uint16_t> w1t((size_t)Hd * 16), w2t((size_t)Hd * Hd), w3p((size_t)Hd * 32);
+        // Device layouts: W1^T [H][16]; W2^T as MFMA A fragments, fragment (b, ks) = lanes
+        // l = 0..63 x 8 values W2[16 ks + 8 (l/32) + i][32 b + l%32]; W3 fragments permuted
+        // to the GEMM2 accumulator layout (see k_epsnet.hip).
+        std::vector<uint16_t> w1t((size_t)Hd * 16), w2f((size_t)Hd * Hd), w3p((size_t)Hd * 32);
         for (int f = 0; f < 16; ++f)
             for (int n = 0; n < Hd; ++n) w1t[(size_t)n * 16 + f] = em->w1[(size_t)f * Hd + n];
-        for (int k = 0; k < Hd; ++k)
-            for (int n = 0; n < Hd; ++n) w2t[(size_t)n * Hd + k] = em->w2[(size_t)k * Hd + n];
+        const int KS = Hd / 16;
+        for (int b = 0; b < Hd / 32; ++b)
+            for (int ks = 0; ks < KS; ++ks)
+                for (int lane = 0; lane < 64; ++lane)
+                    for (int i = 0; i < 8; ++i) {
+                        const int n = b * 32 + (lane & 31), k = ks * 16 + (lane >> 5) * 8 + i;
+                        w2f[(((size_t)b * KS + ks) * 64 + lane) * 8 + i] = em->w2[(size_t)k * Hd + n];
+                    }
         for (int hbg = 0; hbg < Hd / 32; ++hbg)
             for (int jj = 0; jj < 2; ++jj)
                 for (int lane = 0; lane < 64; ++lane)
@@ -311,18 +319,20 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
         __bf16 *w1d, *w2d, *w3d, *wtd;
         double* tvd;
         if ((rc = h->alloc(&w1d, w1t.size(), "w1t"))) return bail(rc);
-        if ((rc = h->alloc(&w2d, w2t.size(), "w2t"))) return bail(rc);
+        if ((rc = h->alloc(&w2d, w2f.size(), "w2f"))) return bail(rc);
         if ((rc = h->alloc(&w3d, w3p.size(), "w3p"))) return bail(rc);
         if ((rc = h->alloc(&wtd, (size_t)em->temb_dim * Hd, "wt"))) return bail(rc);
         if ((rc = h->alloc(&tvd, (size_t)T, "t_values"))) return bail(rc);
         if ((rc = h->alloc(&d.temb, (size_t)T * Hd, "temb"))) return bail(rc);
+        d.nsplit = pa::mlp_splits(Hd);
+        if ((rc = h->alloc(&d.Ep, (size_t)d.nsplit * window * Dz, "Ep"))) return bail(rc);
         PA_HIP_BAIL(hipMemcpyAsync(w1d, w1t.data(), w1t.size() * 2, hipMemcpyHostToDevice, h->stream));
-        PA_HIP_BAIL(hipMemcpyAsync(w2d, w2t.data(), w2t.size() * 2, hipMemcpyHostToDevice, h->stream));
+        PA_HIP_BAIL(hipMemcpyAsync(w2d, w2f.data(), w2f.size() * 2, hipMemcpyHostToDevice, h->stream));
         PA_HIP_BAIL(hipMemcpyAsync(w3d, w3p.data(), w3p.size() * 2, hipMemcpyHostToDevice, h->stream));
         PA_HIP_BAIL(hipMemcpyAsync(wtd, em->wt, (size_t)em->temb_dim * Hd * 2, hipMemcpyHostToDevice, h->stream));
         PA_HIP_BAIL(hipMemcpyAsync(tvd, tv.data(), (size_t)T * sizeof(double), hipMemcpyHostToDevice, h->stream));
         d.w1t = w1d;
-        d.w2t = w2d;
+        d.w2f = w2d;
         d.w3p = w3d;
         PA_HIP_BAIL(pa::launch_temb_table(d, tvd, wtd, em->temb_dim, h->stream));
         PA_HIP_BAIL(hipStreamSynchronize(h->stream));   // host staging vectors die here

@@ -79,7 +79,8 @@ def test_create_rejects_invalid_arguments(kw, frag):
     dict(kind=B.PA_EPS_PATCH_MLP, hidden=768),
     dict(kind=B.PA_EPS_PATCH_MLP, patch=4),
     dict(kind=B.PA_EPS_PATCH_MLP, temb_dim=64),
-    dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 4, 10, 10)),   # 25 tokens: not a multiple of 64
+    dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 4, 10, 10)),   # 25 tokens: not a multiple of 128
+    dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 4, 16, 16)),   # 64 tokens
     dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 3, 16, 16)),
 ])
 def test_create_reports_unbuilt_shapes(kw):
