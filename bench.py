@@ -29,6 +29,27 @@ PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
 PRIMARY_DELTA = 0.05
 
 
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_eps_mlp_traffic_sd_4x64x64_T100_P32_H1024.md")
+
+
+def measured_traffic():
+    """HBM bytes per launch of the network kernel from the committed counter summary, or None
+    when the kernel sources changed since the counters were taken."""
+    import hashlib
+    import re
+    try:
+        text = open(TRAFFIC_RECORD).read()
+        rec = json.loads(re.search(r"```json\n(.*?)```", text, re.S).group(1))
+        h = hashlib.sha256()
+        for src in rec["sources"]:
+            h.update(open(os.path.join(ROOT, src), "rb").read())
+        if h.hexdigest() != rec["source_sha256"]:
+            return None
+        return rec["traffic_bytes_per_launch"]
+    except (OSError, AttributeError, KeyError, ValueError):
+        return None
+
+
 def flops_per_eval(wl) -> float:
     """Algorithmic FLOPs of one patch-MLP evaluation: 2 * tokens * (16 H + H^2 + 16 H)."""
     H = wl.hidden
@@ -175,7 +196,8 @@ def main():
                       for d, r in per_delta.items()},
         "roofline": {"bound": "mfma", "kernel": "k_eps_mlp<1024>",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
+                     "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "avg_launch_us": 1e3 * p["eps_ms"] / max(p["launches"], 1),
                      "flops_per_launch": p["nfe"] * fpe / max(p["launches"], 1)},
     }

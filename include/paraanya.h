@@ -151,7 +151,8 @@ PA_API int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_sc
                            void* stream, uint32_t flags, paraanya_t** out);
 
 /* Start a new sample: state 0 <- x_init (device, D fp32, read on the stream), every cache
- * entry invalid, window [0, min(P, T)), counters zero. Asynchronous. */
+ * entry invalid, window [0, min(P, T)), counters zero. Waits for the handle's earlier work
+ * on the stream, then enqueues the reset and returns without waiting for it. */
 PA_API int paraanya_reset(paraanya_t* h, const float* x_init);
 
 /* Enqueue one sweep (steps (1)-(6) above). If done != NULL the stream is synchronized and
@@ -160,7 +161,9 @@ PA_API int paraanya_reset(paraanya_t* h, const float* x_init);
 PA_API int paraanya_sweep(paraanya_t* h, int32_t* done);
 
 /* reset, sweeps until done, then x_out (device, D fp32) <- state T. Returns after x_out
- * is written (the stream is synchronized). x_init and x_out may alias. */
+ * is written (the stream is synchronized). x_init and x_out may alias. The host does not
+ * synchronize per sweep: it follows a progress word that each sweep writes to pinned host
+ * memory and keeps a few sweeps queued ahead; sweeps queued past the end exit at once. */
 PA_API int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out);
 
 /* Counters and window position; synchronizes the stream. STATE before the first reset. */

@@ -25,6 +25,8 @@
 // use the same lane->slot convention, so any consistent slot->k assignment is valid.
 #include <math.h>
 
+#include <hip/hip_ext.h>
+
 #include "pa_device.h"
 
 namespace pa {
@@ -270,13 +272,13 @@ int mlp_splits(int hidden) { return hidden / kNH; }
 
 int mlp_grid_size(int device_cus) { return device_cus > 0 ? device_cus : 256; }
 
-hipError_t launch_eps_mlp(const Dev& d, hipStream_t st) {
+hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
     switch (d.hidden) {
         case 512:
-            hipLaunchKernelGGL(k_eps_mlp<512>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, d);
+            hipExtLaunchKernelGGL(k_eps_mlp<512>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, start, stop, 0, d);
             break;
         case 1024:
-            hipLaunchKernelGGL(k_eps_mlp<1024>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, d);
+            hipExtLaunchKernelGGL(k_eps_mlp<1024>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, start, stop, 0, d);
             break;
         default:
             return hipErrorInvalidValue;

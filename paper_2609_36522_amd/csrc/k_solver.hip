@@ -325,6 +325,11 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
         ctrl->done = s2 >= d.T;
         ctrl->sweep += 1;
         s_next = s2;
+        // Progress word for the host's launch loop (pinned host memory, system scope; the
+        // host only reads this word and synchronizes the stream before reading anything else).
+        const uint64_t word = ((uint64_t)(uint32_t)ctrl->sweep << 32) |
+                              ((uint64_t)(s2 >= d.T) << 31) | (uint64_t)(uint32_t)min(s2, d.T);
+        __hip_atomic_store(d.progress, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
     __syncthreads();
     const int s2 = s_next;

@@ -42,6 +42,7 @@ struct Dev {
     double* part_res;          // [P][picard_blocks] fp64 partial sums of Eq. (2) residuals
     double* part_dev;          // [P][picard_blocks] fp64 partial sums of Eq. (4) deviations
     Ctrl* ctrl;
+    uint64_t* progress;        // host-mapped word: completed sweeps << 32 | done << 31 | s
     pa_sweep_trace_t* trace;   // [T] or null
     // patch-MLP weights in device layouts
     const __bf16* w1t;         // [hidden][16]     (transposed W1)
@@ -58,7 +59,7 @@ struct Dev {
 hipError_t launch_reset(const Dev& d, hipStream_t st);
 hipError_t launch_slide(const Dev& d, hipStream_t st);
 hipError_t launch_picard(const Dev& d, hipStream_t st, int linear);
-hipError_t launch_eps_mlp(const Dev& d, hipStream_t st);
+hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_temb_table(const Dev& d, const double* t_values_dev, const __bf16* wt_dev,
                              int temb_dim, hipStream_t st);
 int picard_blocks(int D);

@@ -52,6 +52,8 @@ struct paraanya {
     int temb_dim = 0;
     std::vector<double> coef_host;    // [T][2] as uploaded
     Ctrl* ctrl_host = nullptr;        // pinned mirror
+    uint64_t* progress_host = nullptr; // pinned, device-mapped progress word (see k_slide)
+    bool ctrl_fresh = false;           // ctrl_host matches the device and nothing is queued
     bool have_reset = false;
     bool host_done = false;           // done flag of the last synchronized read
     std::vector<void*> allocs;        // device allocations
@@ -66,6 +68,7 @@ struct paraanya {
         for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
         for (void* p : allocs) (void)hipFree(p);
         if (ctrl_host) (void)hipHostFree(ctrl_host);
+        if (progress_host) (void)hipHostFree(progress_host);
     }
 
     template <class T>
@@ -83,9 +86,12 @@ struct paraanya {
     }
 
     int read_ctrl() {
+        // The mirror stays valid until the next enqueue, so repeated queries cost nothing.
+        if (ctrl_fresh) return PA_OK;
         PA_HIP(hipMemcpyAsync(ctrl_host, d.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, stream));
         PA_HIP(hipStreamSynchronize(stream));
         host_done = ctrl_host->done != 0;
+        ctrl_fresh = true;
         return PA_OK;
     }
 
@@ -104,7 +110,8 @@ struct paraanya {
     int next_event(hipEvent_t* out) {
         if (ev_used == ev_pool.size()) {
             hipEvent_t e;
-            PA_HIP(hipEventCreate(&e));
+            // Timing only: no system-scope fence, so the events do not disturb the stream.
+            PA_HIP(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
             ev_pool.push_back(e);
         }
         *out = ev_pool[ev_used++];
@@ -113,17 +120,18 @@ struct paraanya {
 
     int enqueue_sweep() {
         // The miss list of this sweep was published by the previous k_slide (or k_reset).
+        ctrl_fresh = false;
         if (model == PA_EPS_PATCH_MLP) {
+            // Under PROFILE the network launch carries its own start/stop events (no marker
+            // packets between kernels).
             hipEvent_t e0 = nullptr, e1 = nullptr;
             if (flags & PA_FLAG_PROFILE) {
                 int rc = next_event(&e0);
                 if (rc) return rc;
                 rc = next_event(&e1);
                 if (rc) return rc;
-                PA_HIP(hipEventRecord(e0, stream));
             }
-            PA_HIP(pa::launch_eps_mlp(d, stream));
-            if (flags & PA_FLAG_PROFILE) PA_HIP(hipEventRecord(e1, stream));
+            PA_HIP(pa::launch_eps_mlp(d, stream, e0, e1));
         }
         PA_HIP(pa::launch_picard(d, stream, model == PA_EPS_LINEAR));
         PA_HIP(pa::launch_slide(d, stream));
@@ -275,6 +283,11 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     he = hipHostMalloc((void**)&h->ctrl_host, sizeof(Ctrl), hipHostMallocDefault);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostMalloc"));
     memset(h->ctrl_host, 0, sizeof(Ctrl));
+    he = hipHostMalloc((void**)&h->progress_host, 256, hipHostMallocMapped | hipHostMallocCoherent);
+    if (he != hipSuccess) return bail(hip_fail(he, "hipHostMalloc(progress)"));
+    *h->progress_host = 0;
+    he = hipHostGetDevicePointer((void**)&d.progress, h->progress_host, 0);
+    if (he != hipSuccess) return bail(hip_fail(he, "hipHostGetDevicePointer"));
 
 #define PA_HIP_BAIL(call)                                        \
     do {                                                         \
@@ -345,6 +358,10 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
 int paraanya_reset(paraanya_t* h, const float* x_init) {
     g_err.clear();
     if (!h || !x_init) return fail(PA_ERR_INVALID_ARG, "NULL argument");
+    // No kernel of this handle may still publish progress from an earlier sample.
+    PA_HIP(hipStreamSynchronize(h->stream));
+    *h->progress_host = 0;
+    h->ctrl_fresh = false;
     PA_HIP(hipMemcpyAsync(h->d.X, x_init, (size_t)h->d.D * sizeof(float), hipMemcpyDeviceToDevice, h->stream));
     PA_HIP(pa::launch_reset(h->d, h->stream));
     h->have_reset = true;
@@ -376,24 +393,44 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
     int rc = paraanya_reset(h, x_init);
     if (rc) return rc;
     const int T = h->d.T, P = h->d.P;
-    int s_known = 0;
-    int64_t enqueued = 0;
-    for (;;) {
-        // The window start advances by at most P per sweep, so at least ceil((T - s)/P)
-        // more sweeps are needed: enqueue exactly that many before reading back.
-        const int n = (T - s_known + P - 1) / P;
-        for (int i = 0; i < n; ++i)
-            if ((rc = h->enqueue_sweep())) return rc;
-        enqueued += n;
-        if ((rc = h->read_ctrl())) return rc;
-        if (h->ctrl_host->done) break;
-        if (enqueued >= T || h->ctrl_host->s <= s_known)
-            return fail(PA_ERR_HIP, "sampler made no progress (s = %d)", h->ctrl_host->s);
-        s_known = h->ctrl_host->s;
+    // Launch loop without per-sweep synchronisation: k_slide publishes (completed sweeps,
+    // done, s) to a pinned host word after every sweep; the host keeps enough sweeps in
+    // flight -- at least the kLookahead next ones and at least the ceil((T - s)/P) that are
+    // certainly still needed (s advances by at most P per sweep) -- and stops enqueuing once
+    // done is seen. Sweeps enqueued after done exit at their first instruction. Every sweep
+    // advances s by at least 1, so at most T sweeps are ever enqueued. The stream is polled
+    // while waiting, so a failed or idle stream ends the loop.
+    constexpr int kLookahead = 2;
+    volatile uint64_t* prog = h->progress_host;
+    int enqueued = 0;
+    for (unsigned spin = 0;; ++spin) {
+        const uint64_t w = *prog;
+        const int completed = (int)(w >> 32), s_now = (int)(w & 0x7fffffffu);
+        if ((w >> 31) & 1u) break;
+        const int need = (T - s_now + P - 1) / P;
+        const int want = completed + (need > kLookahead ? need : kLookahead);
+        if (enqueued < want && enqueued < T) {
+            const int n = (want < T ? want : T) - enqueued;
+            for (int i = 0; i < n; ++i)
+                if ((rc = h->enqueue_sweep())) return rc;
+            enqueued += n;
+            continue;
+        }
+        if (spin % 256 != 255) continue;        // poll the stream now and then, not per spin
+        const hipError_t q = hipStreamQuery(h->stream);
+        if (q == hipSuccess) {
+            // Stream idle: the word is final for the enqueued work.
+            if ((*prog >> 31) & 1u) break;
+            if (enqueued >= T) return fail(PA_ERR_HIP, "sampler did not finish within T sweeps");
+        } else if (q != hipErrorNotReady) {
+            return hip_fail(q, "hipStreamQuery");
+        }
     }
+    // One synchronization for the output copy and the counters.
     PA_HIP(hipMemcpyAsync(x_out, h->d.X + (size_t)T * h->d.D, (size_t)h->d.D * sizeof(float),
                           hipMemcpyDeviceToDevice, h->stream));
-    PA_HIP(hipStreamSynchronize(h->stream));
+    h->ctrl_fresh = false;
+    if ((rc = h->read_ctrl())) return rc;
     if (h->ctrl_host->nonfinite) return fail(PA_ERR_NONFINITE, "non-finite residual during sampling");
     return PA_OK;
 }
