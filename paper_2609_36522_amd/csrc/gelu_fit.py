@@ -17,8 +17,8 @@ from __future__ import annotations
 import numpy as np
 from scipy.special import erf, erfc
 
-A_MAX = 5.5
-DEG = 10
+A_MAX = 5.0
+DEG = 6
 
 
 def fit(deg=DEG, amax=A_MAX, iters=60):

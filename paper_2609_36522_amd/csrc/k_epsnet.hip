@@ -45,23 +45,19 @@ constexpr int kFeat = 16;               // 2x2 patch x 4 channels
 constexpr int kXRow = kFeat + 8;        // padded LDS row of the token tile (bf16)
 
 // erf-GELU, x * Phi(x) = max(x, 0) - a Q(a) with a = |x| and Q the normal upper tail,
-// branch-free. Q(a) = 2^(-P(min(a, 5.5))) with P a degree-10 polynomial fitted toward the
-// minimax relative error of Q (derivation: gelu_fit.py). One v_exp_f32 and eleven FMA-class
-// instructions per element; in fp32 the result is within 1.4e-7 max(1, |x|) of the exact
-// erf GELU and within 3e-7 (x > 0) / 1.5e-6 (x < 0) relative, well below the bf16 rounding
-// that follows.
+// branch-free. Q(a) = 2^(-P(min(a, 5))) with P a degree-6 polynomial fitted toward the
+// minimax relative error of Q (derivation: gelu_fit.py). One v_exp_f32 and seven FMA-class
+// instructions per element; in fp32 the result is within 2.0e-6 max(1, |x|) of the exact
+// erf GELU and within 1.1e-5 (x > 0) / 1.4e-5 (x < 0) relative. Every GELU output is rounded
+// to bf16 next (relative step 2^-8), so a higher degree buys no accuracy that survives.
 __device__ __forceinline__ float gelu_erf(float x) {
-    const float a = fminf(fabsf(x), 5.5f);
-    float p = fmaf(a, 1.7772681104588628e-08f, -5.619335752271581e-07f);
-    p = fmaf(p, a, 7.6224991971685085e-06f);
-    p = fmaf(p, a, -5.5895987316034734e-05f);
-    p = fmaf(p, a, 0.00020456546917557716f);
-    p = fmaf(p, a, 0.00016647430311422795f);
-    p = fmaf(p, a, -0.007166667375713587f);
-    p = fmaf(p, a, 0.05260409414768219f);
-    p = fmaf(p, a, 0.4591609537601471f);
-    p = fmaf(p, a, 1.1511125564575195f);
-    p = fmaf(p, a, 0.9999998211860657f);
+    const float a = fminf(fabsf(x), 5.0f);
+    float p = fmaf(a, -2.945823871414177e-05f, 0.0007087842677719891f);
+    p = fmaf(p, a, -0.007746023125946522f);
+    p = fmaf(p, a, 0.05260632187128067f);
+    p = fmaf(p, a, 0.4596254229545593f);
+    p = fmaf(p, a, 1.150867223739624f);
+    p = fmaf(p, a, 1.0000176429748535f);
     const float q = __builtin_amdgcn_exp2f(-p);
     return fmaf(-fabsf(x), q, fmaxf(x, 0.0f));
 }
@@ -179,7 +175,10 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         for (int kc = 0; kc < KCH; ++kc) {
             // ---- 2. acc2 += W2^T h1^T over chunk kc (two register stages of W2^T fragments),
             // with chunk kc + 1's h1 slices computed in between (the other wave of the SIMD
-            // can issue VALU while this one waits on the matrix core).
+            // can issue VALU while this one waits on the matrix core). A wave raises its issue
+            // priority while it feeds MFMA groups: the two waves of a SIMD then drift out of
+            // step, one in its MFMA group while the other is in its GELU slice (measured: 12%
+            // faster at 25 misses; without it both run their MFMA and VALU phases together).
             const bool more = kc + 1 < KCH;
             if (more) h1_setup(kc + 1);
             __bf16* nbuf = h1s[(kc + 1) & 1];
@@ -212,12 +211,16 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                 const int kb = 2 * it;
                 load_a(A1, kb + 1);
                 __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_setprio(1);
                 mma(A0, kb);
+                __builtin_amdgcn_s_setprio(0);
                 if (more) h1_slice(nbuf, it);
                 __builtin_amdgcn_sched_barrier(0);
                 load_a(A0, kb + 2 < KBC ? kb + 2 : KBC - 1);
                 __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_setprio(1);
                 mma(A1, kb + 1);
+                __builtin_amdgcn_s_setprio(0);
                 __builtin_amdgcn_sched_barrier(0);
             }
             __syncthreads();                 // chunk kc + 1 complete; chunk kc's buffer free
