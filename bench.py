@@ -8,6 +8,14 @@ One step = one complete sample (every sweep until the window reaches T) through 
 value = sweeps/s at delta = 0.05; eps evals/s and NFE saved against delta = 0 are reported
 beside it, as are the other cache tolerances of the sweep {0, 0.02, 0.05, 0.1}.
 
+Beside the headline line (same JSON object, extra keys):
+  revisit_statistic  the delta = 0 run's fraction of requested drift evaluations that
+                     revisit a timestep whose input moved by less than 0.05 (Sec. 1);
+  batched            8 samples per handle at the same workload (one network launch per
+                     sweep serves every sample's misses): samples/s, eps evals/s;
+  ddpm_window64      ancestral DDPM (eta = 1, pre-drawn step noise) over T = 1000 with a
+                     window of 64 on the same latent and network, delta in {0, 0.05}.
+
 Prints one JSON line (rank 0). The roofline object describes the dominant kernel (the fused
 patch-MLP network kernel): achieved = algorithmic FLOPs of its launches / their summed
 duration, timed with HIP events on the sampler's stream inside the timed region.
@@ -63,6 +71,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--deltas", type=str, default="0,0.02,0.05,0.1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="skip the revisit, batched and DDPM measurements")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle's bounded sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -75,7 +85,7 @@ def timed_samples(sampler, x, steps, warmup, torch):
     for _ in range(warmup):                         # untimed warm-up generations
         sampler.sample(x, out)
     torch.cuda.synchronize()
-    sweeps = nfe = hits = 0
+    sweeps = nfe = hits = revisits = below = 0
     eps_ms = 0.0
     launches = 0
     t0 = time.perf_counter()
@@ -86,12 +96,29 @@ def timed_samples(sampler, x, steps, warmup, torch):
         sweeps += st["sweeps"]
         nfe += st["nfe"]
         hits += st["hits"]
+        revisits += st["revisits"]
+        below += st["revisits_below"]
         eps_ms += kt["eps_ms_total"]
         launches += kt["launches"]
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     return {"seconds": dt, "sweeps": sweeps, "nfe": nfe, "hits": hits, "eps_ms": eps_ms,
-            "launches": launches, "out": out}
+            "launches": launches, "revisits": revisits, "revisits_below": below, "out": out}
+
+
+def run_case(wl, delta, steps, warmup, torch, weights, *, batch=1, eta=0.0):
+    """Timed samples of one configuration (profiled handle: kernel-attached events)."""
+    from paper_2609_36522_amd import binding, inputs
+    if batch == 1:
+        xs = inputs.x_init(wl.latent).reshape(-1)
+    else:
+        xs = inputs.x_init_batch(wl.latent, batch).reshape(-1)
+    x = torch.from_numpy(xs).cuda()
+    with binding.from_workload(wl, delta, seed_weights=weights, profile=True, batch=batch,
+                               eta=eta) as s:
+        if eta > 0:
+            s.set_noise(torch.from_numpy(inputs.step_noise(batch, wl.T, wl.D).reshape(-1)).cuda())
+        return timed_samples(s, x, steps, warmup, torch)
 
 
 def cpu_baseline(wl, delta, budget_s):
@@ -135,18 +162,60 @@ def main():
     deltas = [float(v) for v in args.deltas.split(",")]
     if PRIMARY_DELTA not in deltas:
         deltas.append(PRIMARY_DELTA)
-    x = torch.from_numpy(inputs.x_init(wl.latent).reshape(-1)).cuda()
     weights = inputs.mlp_weights(wl.hidden, temb_dim=wl.temb_dim)
     fpe = flops_per_eval(wl)
 
     per_delta = {}
     for d in deltas:
-        with binding.from_workload(wl, d, seed_weights=weights, profile=True) as s:
-            r = timed_samples(s, x, args.steps, args.warmup, torch)
+        r = run_case(wl, d, args.steps, args.warmup, torch, weights)
         per_delta[d] = r
         print(f"[bench] delta={d}: {r['sweeps'] / args.steps:.1f} sweeps/sample, "
               f"NFE {r['nfe'] / args.steps:.1f}, {1e3 * r['seconds'] / args.steps:.3f} ms/sample",
               file=sys.stderr, flush=True)
+
+    extras = {}
+    if not args.headline_only:
+        # revisit statistic of the delta = 0 run (the cache's motivation figure, Sec. 1)
+        if 0.0 in per_delta:
+            r0 = per_delta[0.0]
+            req = r0["nfe"] + r0["hits"]
+            extras["revisit_statistic"] = {
+                "threshold": 0.05, "delta": 0.0,
+                "fraction_of_requests": r0["revisits_below"] / req,
+                "revisit_fraction": r0["revisits"] / req,
+                "requests_per_sample": req / args.steps}
+        # several samples per handle
+        nb = 8
+        bsteps = max(args.steps // 3, 3)
+        rb = run_case(wl, PRIMARY_DELTA, bsteps, 1, torch, weights, batch=nb)
+        extras["batched"] = {
+            "samples": nb, "delta": PRIMARY_DELTA, "steps": bsteps,
+            "ms_per_batch": 1e3 * rb["seconds"] / bsteps,
+            "samples_per_s": nb * bsteps / rb["seconds"],
+            "eps_evals_per_s": rb["nfe"] / rb["seconds"],
+            "batched_sweeps_per_batch": rb["sweeps"] / bsteps,
+            "nfe_per_sample": rb["nfe"] / (nb * bsteps),
+            "eps_kernel_tflops": (rb["nfe"] * fpe) / (rb["eps_ms"] * 1e-3) / 1e12 if rb["eps_ms"] > 0 else None}
+        print(f"[bench] batch {nb}: {extras['batched']['ms_per_batch']:.3f} ms/batch, "
+              f"{extras['batched']['samples_per_s']:.0f} samples/s", file=sys.stderr, flush=True)
+        # the window study's stochastic setting
+        wd = wl.with_(T=1000, window=64)
+        dsteps = max(args.steps // 6, 3)
+        dd = {}
+        for d in (0.0, PRIMARY_DELTA):
+            r = run_case(wd, d, dsteps, 1, torch, weights, eta=1.0)
+            dd[d] = r
+            print(f"[bench] ddpm T=1000 P=64 delta={d}: {1e3 * r['seconds'] / dsteps:.3f} ms/sample, "
+                  f"NFE {r['nfe'] / dsteps:.0f}", file=sys.stderr, flush=True)
+        extras["ddpm_window64"] = {
+            "T": 1000, "window": 64, "eta": 1.0, "steps": dsteps,
+            "per_delta": {str(d): {"ms_per_sample": 1e3 * r["seconds"] / dsteps,
+                                   "sweeps_per_s": r["sweeps"] / r["seconds"],
+                                   "eps_evals_per_s": r["nfe"] / r["seconds"],
+                                   "nfe_per_sample": r["nfe"] / dsteps,
+                                   "sweeps_per_sample": r["sweeps"] / dsteps}
+                          for d, r in dd.items()},
+            "nfe_saved_vs_delta0": 1.0 - dd[PRIMARY_DELTA]["nfe"] / dd[0.0]["nfe"]}
 
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * (1 << 20) // 4
@@ -201,6 +270,7 @@ def main():
                      "avg_launch_us": 1e3 * p["eps_ms"] / max(p["launches"], 1),
                      "flops_per_launch": p["nfe"] * fpe / max(p["launches"], 1)},
     }
+    line.update(extras)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, PRIMARY_DELTA, args.cpu_seconds)
     print(json.dumps(line), flush=True)

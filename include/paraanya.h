@@ -22,7 +22,10 @@
  *   - Device pointers are HIP device addresses on the handle's current device; host
  *     pointers are ordinary CPU memory. The library never takes ownership of caller
  *     memory: it copies what it needs and owns every buffer it allocates.
- *   - Latents are fp32, batch 1, layout [C][H][W] row-major, D = C*H*W elements.
+ *   - Latents are fp32, layout [N][C][H][W] row-major, D = C*H*W elements per sample.
+ *     N independent samples share one handle (same T, window, thresholds, network): each
+ *     has its own trajectory, cache and window, and one batched sweep advances every sample
+ *     that is not done, with all their misses evaluated by one network launch.
  *   - Sampler state index i = 0..T: state 0 is the initial noise, state T the output.
  */
 #ifndef PARAANYA_H
@@ -50,6 +53,7 @@ extern "C" {
 #define PA_ERR_UNSUPPORTED (-6)  /* valid request this build does not implement */
 
 #define PA_MAX_WINDOW 256        /* largest window P */
+#define PA_MAX_BATCH  64         /* largest number of samples N per handle */
 
 /* ------------------------------------------------------------------ schedule */
 #define PA_SCHED_SCALED_LINEAR 0
@@ -62,7 +66,13 @@ extern "C" {
  * t_j = round(train_steps - j*train_steps/T) - 1, alpha_bar of the final state = 1
  * (final_alpha_one must be 1). EXPLICIT: the caller gives alpha_bar[0..T] (host, state
  * order, alpha_bar[T] is the clean end) and t_values[0..T-1] (host; used only for the
- * time embedding of the patch-MLP). Copied at create. */
+ * time embedding of the patch-MLP). Copied at create.
+ * eta in [0, 1] selects the step (the generalized DDIM step of the DDIM paper):
+ * x_{i+1} = sqrt(ab_{i+1}) x0^ + sqrt(1 - ab_{i+1} - sigma_i^2) eps + sigma_i z_i with
+ * sigma_i = eta sqrt((1 - ab_{i+1}) / (1 - ab_i)) sqrt(1 - ab_i / ab_{i+1}). eta = 0 is
+ * deterministic DDIM; eta = 1 is ancestral DDPM sampling (the stochastic sampler of the
+ * paper's window study, Sec. 3.4), whose per-step noise z_i is drawn before sampling and
+ * given with paraanya_set_noise, so that Picard iteration solves a fixed recurrence. */
 typedef struct {
     int32_t kind;
     double beta_start, beta_end;
@@ -71,6 +81,7 @@ typedef struct {
     int32_t final_alpha_one;
     const double* alpha_bar;
     const int32_t* t_values;
+    double eta;
 } pa_schedule_t;
 
 /* ------------------------------------------------------------------ noise network */
@@ -106,7 +117,16 @@ typedef struct {
 typedef struct paraanya paraanya_t;
 
 /* Counters of Sec. 3.1 / Tab. cache_tol: nfe = single-latent network evaluations (the
- * misses), hits = window slots served from the cache, sweeps = Picard iterations. */
+ * misses), hits = window slots served from the cache, sweeps = Picard iterations.
+ * revisits / revisits_below feed the revisit statistic of Sec. 1: of all requested drift
+ * evaluations (nfe + hits, one per window slot and sweep), revisits are those at a
+ * timestep evaluated before, and revisits_below those whose input moved by less than the
+ * revisit threshold (Eq. (4) deviation from the cached input; paraanya_set_revisit_threshold,
+ * default 0.05). Run at delta = 0, revisits_below / (nfe + hits) is the fraction of
+ * requested evaluations that a cache with tolerance equal to the threshold would first
+ * target. For a batched handle paraanya_stats sums the counters over the samples and
+ * reports sweeps = the largest per-sample count, window_start/window_end = the smallest
+ * per-sample values, done = all samples done, nonfinite = any. */
 typedef struct {
     int64_t nfe;
     int64_t hits;
@@ -116,6 +136,8 @@ typedef struct {
     int32_t window_end;   /* e = min(s + P, T) */
     int32_t done;         /* s >= T */
     int32_t nonfinite;    /* a non-finite residual was seen (sticky until reset) */
+    int64_t revisits;
+    int64_t revisits_below;
 } pa_stats_t;
 
 /* One sweep's decisions (test hook). Slot j <-> timestep s + j, j < e - s. */
@@ -136,42 +158,60 @@ typedef struct {
 
 /* ------------------------------------------------------------------ entry points */
 
-/* Create a sampler. latent_shape = {N, C, H, W} with N = 1; T >= 1 sampling steps;
+/* Create a sampler. latent_shape = {N, C, H, W} with 1 <= N <= PA_MAX_BATCH samples; T >= 1 sampling steps;
  * window P in [1, min(T, PA_MAX_WINDOW)]; delta >= 0 the cache tolerance of Eq. (5)
  * (strict '<'; 0 disables hits; +inf allowed); tol >= 0 the tau of Eq. (2) (mean
  * square, '<='). Both thresholds are compared against fp64 sums: states and network
  * outputs are stored in fp32, and the drift, the Picard sum, the deviations and the
  * residuals are computed in fp64 from them, then rounded once on store. stream is a hipStream_t (NULL = the null stream). On success *out
  * holds the handle; on failure *out = NULL and nothing is left allocated.
- * Errors: INVALID_ARG (N != 1, C*H*W % 4 != 0, T < 1, window outside range, delta or tol
- * negative/NaN, bad schedule or model fields), UNSUPPORTED (model shape not built),
- * OOM, HIP. */
+ * Errors: INVALID_ARG (N outside [1, PA_MAX_BATCH], C*H*W % 4 != 0, T < 1, window outside
+ * range, delta or tol negative/NaN, eta outside [0, 1], bad schedule or model fields),
+ * UNSUPPORTED (model shape not built), OOM, HIP. */
 PA_API int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_t* schedule,
                            int32_t window, double delta, double tol, const pa_eps_model_t* eps_model,
                            void* stream, uint32_t flags, paraanya_t** out);
 
-/* Start a new sample: state 0 <- x_init (device, D fp32, read on the stream), every cache
- * entry invalid, window [0, min(P, T)), counters zero. Waits for the handle's earlier work
- * on the stream, then enqueues the reset and returns without waiting for it. */
+/* Start new samples: state 0 of sample n <- x_init[n] (device, N x D fp32, read on the
+ * stream), every cache entry invalid, windows [0, min(P, T)), counters zero. Waits for the
+ * handle's earlier work on the stream, then enqueues the reset and returns without waiting
+ * for it. STATE if eta > 0 and no noise was given (paraanya_set_noise). */
 PA_API int paraanya_reset(paraanya_t* h, const float* x_init);
 
-/* Enqueue one sweep (steps (1)-(6) above). If done != NULL the stream is synchronized and
- * *done receives the done flag. Errors: STATE (before reset, or the last synchronized
- * state was already done), NONFINITE (only when done != NULL and a residual was NaN/Inf). */
+/* Pre-sampled per-step noise of the stochastic sampler (eta > 0): z (device, N x T x D
+ * fp32, layout [n][i][D], i the sampling step) is copied on the stream into the handle and
+ * used by every following sample until replaced; sigma_i z_i is added to the drift of
+ * step i. INVALID_ARG for eta = 0 handles or z == NULL. */
+PA_API int paraanya_set_noise(paraanya_t* h, const float* z);
+
+/* Threshold of the revisit statistic (see pa_stats_t); >= 0, +inf allowed; applies to the
+ * sweeps enqueued after the call. */
+PA_API int paraanya_set_revisit_threshold(paraanya_t* h, double threshold);
+
+/* Enqueue one sweep (steps (1)-(6) above) of every sample not yet done. If done != NULL
+ * the stream is synchronized and *done receives 1 once every sample is done. Errors: STATE
+ * (before reset, or the last synchronized state was already done), NONFINITE (only when
+ * done != NULL and a residual was NaN/Inf). */
 PA_API int paraanya_sweep(paraanya_t* h, int32_t* done);
 
-/* reset, sweeps until done, then x_out (device, D fp32) <- state T. Returns after x_out
+/* reset, sweeps until every sample is done, then x_out (device, N x D fp32) <- state T of
+ * each sample. Returns after x_out
  * is written (the stream is synchronized). x_init and x_out may alias. The host does not
  * synchronize per sweep: it follows a progress word that each sweep writes to pinned host
  * memory and keeps a few sweeps queued ahead; sweeps queued past the end exit at once. */
 PA_API int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out);
 
-/* Counters and window position; synchronizes the stream. STATE before the first reset. */
+/* Counters and window position; synchronizes the stream. STATE before the first reset.
+ * paraanya_stats aggregates over the samples (see pa_stats_t); paraanya_stats_sample
+ * reports sample n alone (INVALID_ARG for n outside [0, N)). */
 PA_API int paraanya_stats(paraanya_t* h, pa_stats_t* out);
+PA_API int paraanya_stats_sample(paraanya_t* h, int32_t n, pa_stats_t* out);
 
 /* Trace record of sweep k (0-based) since reset; needs PA_FLAG_TRACE. Synchronizes.
- * INVALID_ARG if k is not a completed sweep; STATE without the flag. */
+ * INVALID_ARG if k is not a completed sweep of that sample or n is out of range; STATE
+ * without the flag. paraanya_trace is sample 0. */
 PA_API int paraanya_trace(paraanya_t* h, int32_t k, pa_sweep_trace_t* out);
+PA_API int paraanya_trace_sample(paraanya_t* h, int32_t n, int32_t k, pa_sweep_trace_t* out);
 
 /* Test hook: copy state rows to host memory; synchronizes. Any pointer may be NULL.
  * X receives states [t0, t1) (t1 <= T+1); Xh, Eh, valid receive cache rows [t0, min(t1, T)).
@@ -179,12 +219,16 @@ PA_API int paraanya_trace(paraanya_t* h, int32_t k, pa_sweep_trace_t* out);
  * newest computed state (the window start's row shows which rows were computed). */
 PA_API int paraanya_read_state(paraanya_t* h, int32_t t0, int32_t t1, float* X, float* Xh,
                         float* Eh, uint8_t* valid);
+/* The same for sample n (paraanya_read_state is sample 0). */
+PA_API int paraanya_read_state_sample(paraanya_t* h, int32_t n, int32_t t0, int32_t t1, float* X,
+                                      float* Xh, float* Eh, uint8_t* valid);
 
-/* Test hook: the fp64 DDIM coefficients the device uses, alpha[i] = a_i - 1 and b[i]
- * (host arrays of T), with d_i = alpha_i x_i + b_i eps_i, a_i = sqrt(ab_{i+1}/ab_i),
- * b_i = sqrt(1 - ab_{i+1}) - a_i sqrt(1 - ab_i); and, for the patch-MLP, the fp32
- * time-embedding table e[T][hidden] (host, may be NULL). */
-PA_API int paraanya_coefficients(paraanya_t* h, double* alpha, double* b, float* temb);
+/* Test hook: the fp64 step coefficients the device uses (host arrays of T, any may be
+ * NULL): alpha[i] = a_i - 1, b[i], sigma[i], with the drift d_i = alpha_i x_i + b_i eps_i
+ * + sigma_i z_i, a_i = sqrt(ab_{i+1}/ab_i), b_i = sqrt(1 - ab_{i+1} - sigma_i^2)
+ * - a_i sqrt(1 - ab_i) and sigma_i as under pa_schedule_t; and, for the patch-MLP, the
+ * fp32 time-embedding table e[T][hidden]. */
+PA_API int paraanya_coefficients(paraanya_t* h, double* alpha, double* b, double* sigma, float* temb);
 
 /* Network-launch timings since reset (PA_FLAG_PROFILE); synchronizes. STATE without it. */
 PA_API int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out);

@@ -16,6 +16,10 @@ Readings where the paper is silent (the design doc lists them as R1-R20):
 * states that enter the window start as copies of the newest computed state;
 * misses are listed in ascending t; hit test is strict '<' (Eq. (5)).
 
+Stochastic steps (reading R21): with pre-drawn step noise z_i and scale sigma_i the drift
+gains the term sigma_i z_i, which is the same in every sweep; ``noise`` below is the array
+of those terms, [T, D] (None for the deterministic sampler).
+
 Storage is ``store_dtype`` (fp32 like the device, or fp64 for closed-form checks); all
 arithmetic is float64 with one rounding on store.
 """
@@ -102,15 +106,23 @@ def cache_update(st: State, M, E) -> None:
         st.valid[t] = True
 
 
-def picard_update(X, Eh, s: int, e: int, alpha, b) -> np.ndarray:
+def step_noise_terms(sigma, Z) -> np.ndarray:
+    """sigma_i z_i for every step i (float64), from the scales and the pre-drawn noise."""
+    return np.asarray(sigma, dtype=F64)[:, None] * np.asarray(Z, dtype=F64)
+
+
+def picard_update(X, Eh, s: int, e: int, alpha, b, noise=None) -> np.ndarray:
     """Eq. (1) over the window, anchored at state s:
-    x_{t+1}^{k+1} = x_s + sum_{i=s}^{t} (alpha_i x_i^k + b_i eps_i^k), t = s..e-1.
+    x_{t+1}^{k+1} = x_s + sum_{i=s}^{t} (alpha_i x_i^k + b_i eps_i^k [+ sigma_i z_i]), t = s..e-1.
     Overwrites X[s+1..e]; returns the Eq. (2) residuals r for states s+1..e."""
     acc = X[s].astype(F64)
     Y = np.empty((e - s, X.shape[1]), dtype=X.dtype)
     for j in range(e - s):
         t = s + j
-        acc = acc + (float(alpha[t]) * X[t].astype(F64) + float(b[t]) * Eh[t].astype(F64))
+        d = float(alpha[t]) * X[t].astype(F64) + float(b[t]) * Eh[t].astype(F64)
+        if noise is not None:
+            d = d + noise[t]
+        acc = acc + d
         Y[j] = acc
     r = np.empty(e - s)
     for j in range(e - s):
@@ -133,7 +145,7 @@ def leading_converged(r, tau: float) -> int:
 
 
 def sweep(st: State, P: int, delta: float, tau: float, alpha, b, eps_fn, *,
-          force_hit=None) -> dict:
+          force_hit=None, noise=None) -> dict:
     """One Picard sweep with the output cache. ``force_hit`` (test hook) replaces the
     hit mask computed by the cache test. Returns the sweep's trace record."""
     T = st.T
@@ -149,7 +161,7 @@ def sweep(st: State, P: int, delta: float, tau: float, alpha, b, eps_fn, *,
         E = eps_fn(st.X[M], M)          # one batched evaluation of the misses
         cache_update(st, M, E)
     # Eq. (6): after the update, Eh[t] is eps^_t for hits and the fresh output for misses.
-    r = picard_update(st.X, st.Eh, s, e, alpha, b)
+    r = picard_update(st.X, st.Eh, s, e, alpha, b, noise)
     c = leading_converged(r, tau)
     s_next = s + 1 + c
     st.nfe += len(M)
@@ -161,19 +173,34 @@ def sweep(st: State, P: int, delta: float, tau: float, alpha, b, eps_fn, *,
 
 
 def sample(x_init, T: int, P: int, delta: float, tau: float, alpha, b, eps_fn,
-           store_dtype=np.float32, max_sweeps=None):
+           store_dtype=np.float32, max_sweeps=None, noise=None):
     """Run sweeps until the window start reaches T. Returns (x_T, trace, state)."""
     st = init_state(x_init, T, store_dtype)
     trace = []
     limit = T if max_sweeps is None else max_sweeps
     while not st.done and st.sweeps < limit:
-        trace.append(sweep(st, P, delta, tau, alpha, b, eps_fn))
+        trace.append(sweep(st, P, delta, tau, alpha, b, eps_fn, noise=noise))
     return st.X[T].copy(), trace, st
+
+
+def revisit_counts(trace, threshold: float):
+    """The revisit statistic of Sec. 1 over a run's trace: (requested evaluations, revisits,
+    revisits whose Eq. (4) deviation from the cached input is below ``threshold``). A window
+    slot is a requested drift evaluation; it is a revisit if its timestep holds a cache
+    entry (its deviation is a number, not NaN)."""
+    requests = revisits = below = 0
+    for rec in trace:
+        dev = np.asarray(rec["dev"], dtype=F64)
+        requests += dev.size
+        seen = ~np.isnan(dev)
+        revisits += int(np.count_nonzero(seen))
+        below += int(np.count_nonzero(dev[seen] < threshold))
+    return requests, revisits, below
 
 
 # --------------------------------------------------------------------------- references
 def picard_uncached(x_init, T: int, P: int, tau: float, alpha, b, eps_fn,
-                    store_dtype=np.float32):
+                    store_dtype=np.float32, noise=None):
     """Sliding-window Picard with no cache: every window timestep is evaluated each sweep.
     Same readings as :func:`sweep`; shares none of the cache code."""
     X = np.zeros((T + 1, np.asarray(x_init).size), dtype=store_dtype)
@@ -191,6 +218,8 @@ def picard_uncached(x_init, T: int, P: int, tau: float, alpha, b, eps_fn,
         Y = np.empty((e - s, X.shape[1]), dtype=store_dtype)
         for j, t in enumerate(steps):
             acc = acc + (float(alpha[t]) * X[t].astype(F64) + float(b[t]) * E[j].astype(F64))
+            if noise is not None:
+                acc = acc + noise[t]
             Y[j] = acc
         r = np.array([float(np.mean((Y[j].astype(F64) - X[s + 1 + j].astype(F64)) ** 2))
                       for j in range(e - s)])
@@ -203,13 +232,31 @@ def picard_uncached(x_init, T: int, P: int, tau: float, alpha, b, eps_fn,
     return X[T].copy(), trace, nfe
 
 
-def ddim_serial_drift(x_init, alpha, b, eps_fn, store_dtype=np.float32):
-    """Serial DDIM in drift form: x_{i+1} = x_i + (alpha_i x_i + b_i eps_i)."""
+def ddim_serial_drift(x_init, alpha, b, eps_fn, store_dtype=np.float32, noise=None):
+    """Serial DDIM in drift form: x_{i+1} = x_i + (alpha_i x_i + b_i eps_i [+ sigma_i z_i])."""
     x = np.asarray(x_init, dtype=store_dtype).reshape(-1)
     for i in range(len(alpha)):
         e = eps_fn(x[None, :], [i])[0]
-        x = (x.astype(F64) + (float(alpha[i]) * x.astype(F64) + float(b[i]) * e.astype(F64))
-             ).astype(store_dtype)
+        d = float(alpha[i]) * x.astype(F64) + float(b[i]) * e.astype(F64)
+        if noise is not None:
+            d = d + noise[i]
+        x = (x.astype(F64) + d).astype(store_dtype)
+    return x
+
+
+def ddpm_serial_textbook(x_init, ab, eps_fn, Z, store_dtype=np.float32):
+    """Serial ancestral DDPM in its textbook form over the sampler's states: with
+    beta'_i = 1 - ab_i / ab_{i+1} (the step's beta on the possibly respaced grid),
+    x_{i+1} = (x_i - beta'_i / sqrt(1 - ab_i) eps) / sqrt(1 - beta'_i) + s_i z_i,
+    s_i^2 = beta'_i (1 - ab_{i+1}) / (1 - ab_i) (the posterior variance)."""
+    x = np.asarray(x_init, dtype=store_dtype).reshape(-1)
+    ab = np.asarray(ab, dtype=F64)
+    for i in range(len(ab) - 1):
+        e = eps_fn(x[None, :], [i])[0].astype(F64)
+        beta = 1.0 - ab[i] / ab[i + 1]
+        mean = (x.astype(F64) - beta / np.sqrt(1.0 - ab[i]) * e) / np.sqrt(1.0 - beta)
+        var = beta * (1.0 - ab[i + 1]) / (1.0 - ab[i])
+        x = (mean + np.sqrt(var) * np.asarray(Z[i], dtype=F64)).astype(store_dtype)
     return x
 
 

@@ -13,7 +13,12 @@ the reading used here (readings R1 and R14):
 * deterministic DDIM (eta = 0) from state i to i+1 is x_{i+1} = a_i x_i + b_i eps_i with
   a_i = sqrt(ab_{i+1} / ab_i), b_i = sqrt(1 - ab_{i+1}) - a_i sqrt(1 - ab_i); the
   per-step drift is d_i = x_{i+1} - x_i = alpha_i x_i + b_i eps_i with alpha_i = a_i - 1
-  (the 1/T factor of Eq. (1) is absorbed into the one-step increment).
+  (the 1/T factor of Eq. (1) is absorbed into the one-step increment);
+* the stochastic sampler of the window study (DDPM, Sec. 3.4) is the generalized DDIM step
+  with eta = 1: x_{i+1} = sqrt(ab_{i+1}) x0^ + sqrt(1 - ab_{i+1} - sigma_i^2) eps + sigma_i z_i,
+  sigma_i = eta sqrt((1 - ab_{i+1}) / (1 - ab_i)) sqrt(1 - ab_i / ab_{i+1}), with the noise
+  z_i drawn before sampling so that the Picard iteration solves a fixed recurrence
+  (reading R21).
 
 Everything is float64.
 """
@@ -57,3 +62,16 @@ def ddim_coefficients(ab: np.ndarray):
     alpha = a - 1.0
     b = np.sqrt(1.0 - ab[1:]) - a * np.sqrt(1.0 - ab[:-1])
     return alpha, b
+
+
+def step_coefficients(ab: np.ndarray, eta: float):
+    """(alpha, b, sigma) of the generalized DDIM step with parameter eta, as the one-step
+    increment d_i = alpha_i x_i + b_i eps_i + sigma_i z_i (eta = 0 gives ddim_coefficients)."""
+    ab = np.asarray(ab, dtype=np.float64)
+    ab0, ab1 = ab[:-1], ab[1:]
+    sigma = eta * np.sqrt((1.0 - ab1) / (1.0 - ab0)) * np.sqrt(1.0 - ab0 / ab1)
+    a = np.sqrt(ab1 / ab0)
+    alpha = a - 1.0
+    x0_coef_eps = np.sqrt(1.0 - ab1 - sigma * sigma)
+    b = x0_coef_eps - a * np.sqrt(1.0 - ab0)
+    return alpha, b, sigma

@@ -22,6 +22,7 @@ PA_ERR_STATE = -4
 PA_ERR_NONFINITE = -5
 PA_ERR_UNSUPPORTED = -6
 PA_MAX_WINDOW = 256
+PA_MAX_BATCH = 64
 
 PA_SCHED_SCALED_LINEAR = 0
 PA_SCHED_EXPLICIT = 1
@@ -34,14 +35,15 @@ PA_FLAG_PROFILE = 2
 EXPORTED = ("paraanya_create", "paraanya_reset", "paraanya_sweep", "paraanya_sample",
             "paraanya_stats", "paraanya_trace", "paraanya_read_state", "paraanya_coefficients",
             "paraanya_kernel_times", "paraanya_destroy", "paraanya_last_error",
-            "paraanya_status_str")
+            "paraanya_status_str", "paraanya_set_noise", "paraanya_set_revisit_threshold",
+            "paraanya_stats_sample", "paraanya_trace_sample", "paraanya_read_state_sample")
 
 
 class Schedule(C.Structure):
     _fields_ = [("kind", C.c_int32), ("beta_start", C.c_double), ("beta_end", C.c_double),
                 ("train_steps", C.c_int32), ("spacing", C.c_int32),
                 ("final_alpha_one", C.c_int32), ("alpha_bar", C.POINTER(C.c_double)),
-                ("t_values", C.POINTER(C.c_int32))]
+                ("t_values", C.POINTER(C.c_int32)), ("eta", C.c_double)]
 
 
 class EpsModel(C.Structure):
@@ -54,7 +56,8 @@ class EpsModel(C.Structure):
 class Stats(C.Structure):
     _fields_ = [("nfe", C.c_int64), ("hits", C.c_int64), ("misses", C.c_int64),
                 ("sweeps", C.c_int64), ("window_start", C.c_int32), ("window_end", C.c_int32),
-                ("done", C.c_int32), ("nonfinite", C.c_int32)]
+                ("done", C.c_int32), ("nonfinite", C.c_int32),
+                ("revisits", C.c_int64), ("revisits_below", C.c_int64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -99,9 +102,14 @@ def load_library(path: str = LIB_PATH):
     lib.paraanya_sweep.argtypes = [P, C.POINTER(I32)]
     lib.paraanya_sample.argtypes = [P, P, P]
     lib.paraanya_stats.argtypes = [P, C.POINTER(Stats)]
+    lib.paraanya_stats_sample.argtypes = [P, I32, C.POINTER(Stats)]
     lib.paraanya_trace.argtypes = [P, I32, C.POINTER(SweepTrace)]
+    lib.paraanya_trace_sample.argtypes = [P, I32, I32, C.POINTER(SweepTrace)]
     lib.paraanya_read_state.argtypes = [P, I32, I32, P, P, P, P]
-    lib.paraanya_coefficients.argtypes = [P, P, P, P]
+    lib.paraanya_read_state_sample.argtypes = [P, I32, I32, I32, P, P, P, P]
+    lib.paraanya_coefficients.argtypes = [P, P, P, P, P]
+    lib.paraanya_set_noise.argtypes = [P, P]
+    lib.paraanya_set_revisit_threshold.argtypes = [P, F64]
     lib.paraanya_kernel_times.argtypes = [P, C.POINTER(KTimes)]
     lib.paraanya_destroy.argtypes = [P]
     lib.paraanya_destroy.restype = None
@@ -138,29 +146,33 @@ class Sampler:
     """One handle of the cached Picard sampler.
 
     ``model`` is "linear" (needs ``c``) or "patch_mlp" (needs ``weights`` as a dict of bf16
-    bit-pattern arrays w1, wt, w2, w3). ``stream`` is a torch.cuda.Stream or None (the
-    current stream)."""
+    bit-pattern arrays w1, wt, w2, w3). ``batch`` independent samples share the handle
+    (tensors passed to reset/sample hold batch x D values). ``eta`` > 0 selects the
+    stochastic step (1 = ancestral DDPM); its step noise is given with :meth:`set_noise`.
+    ``stream`` is a torch.cuda.Stream or None (the current stream)."""
 
     def __init__(self, latent, T, window, delta, tol, model, *, c=None, weights=None,
-                 hidden=0, schedule=None, stream=None, trace=False, profile=False):
+                 hidden=0, schedule=None, stream=None, trace=False, profile=False, batch=1,
+                 eta=0.0):
         import torch
         self.lib = load_library()
         self.latent = tuple(int(v) for v in latent)
         self.T, self.P = int(T), int(window)
         self.D = int(np.prod(self.latent))
+        self.N = int(batch)
         self.torch = torch
         self.stream = stream if stream is not None else torch.cuda.current_stream()
-        shape = (C.c_int32 * 4)(1, *self.latent)
+        shape = (C.c_int32 * 4)(self.N, *self.latent)
         self._keep = []
         if schedule is None:
             sc = Schedule(PA_SCHED_SCALED_LINEAR, 0.00085, 0.012, 1000, PA_SPACING_TRAILING, 1,
-                          None, None)
+                          None, None, float(eta))
         else:
             ab = np.ascontiguousarray(schedule["alpha_bar"], dtype=np.float64)
             tv = np.ascontiguousarray(schedule["t_values"], dtype=np.int32)
             self._keep += [ab, tv]
             sc = Schedule(PA_SCHED_EXPLICIT, 0.0, 0.0, 0, 0, 0, _ptr(ab, C.c_double),
-                          _ptr(tv, C.c_int32))
+                          _ptr(tv, C.c_int32), float(eta))
         if model == "linear":
             cc = np.ascontiguousarray(c, dtype=np.float32)
             self._keep.append(cc)
@@ -201,15 +213,23 @@ class Sampler:
         self.close()
 
     # ------------------------------------------------------------------ sampling
-    def _dev(self, x):
+    def _dev(self, x, count=None):
         t = self.torch
+        count = self.N * self.D if count is None else count
         if not (isinstance(x, t.Tensor) and x.is_cuda and x.dtype == t.float32 and x.is_contiguous()
-                and x.numel() == self.D):
-            raise ValueError(f"expected a contiguous fp32 CUDA tensor of {self.D} elements")
+                and x.numel() == count):
+            raise ValueError(f"expected a contiguous fp32 CUDA tensor of {count} elements")
         return C.c_void_p(x.data_ptr())
 
     def reset(self, x_init):
         _check(self.lib.paraanya_reset(self.h, self._dev(x_init)))
+
+    def set_noise(self, z):
+        """Step noise z[n][i][D] (fp32 CUDA tensor) of the stochastic step (eta > 0)."""
+        _check(self.lib.paraanya_set_noise(self.h, self._dev(z, self.N * self.T * self.D)))
+
+    def set_revisit_threshold(self, threshold: float):
+        _check(self.lib.paraanya_set_revisit_threshold(self.h, float(threshold)))
 
     def sweep(self, sync: bool = False):
         if not sync:
@@ -226,40 +246,47 @@ class Sampler:
         return x_out
 
     # ------------------------------------------------------------------ inspection
-    def stats(self) -> dict:
+    def stats(self, n=None) -> dict:
+        """Counters aggregated over the samples, or of sample ``n``."""
         st = Stats()
-        _check(self.lib.paraanya_stats(self.h, C.byref(st)))
+        if n is None:
+            _check(self.lib.paraanya_stats(self.h, C.byref(st)))
+        else:
+            _check(self.lib.paraanya_stats_sample(self.h, int(n), C.byref(st)))
         return st.as_dict()
 
-    def trace(self, k: int) -> dict:
+    def trace(self, k: int, n: int = 0) -> dict:
         tr = SweepTrace()
-        _check(self.lib.paraanya_trace(self.h, int(k), C.byref(tr)))
+        _check(self.lib.paraanya_trace_sample(self.h, int(n), int(k), C.byref(tr)))
         return tr.as_dict()
 
-    def traces(self) -> list:
-        return [self.trace(k) for k in range(self.stats()["sweeps"])]
+    def traces(self, n: int = 0) -> list:
+        return [self.trace(k, n) for k in range(self.stats(n)["sweeps"])]
 
-    def read_state(self, t0: int = 0, t1=None):
-        """Host copies of X[t0:t1], Xh/Eh/valid[t0:min(t1, T)]."""
+    def read_state(self, t0: int = 0, t1=None, n: int = 0):
+        """Host copies of sample n's X[t0:t1], Xh/Eh/valid[t0:min(t1, T)]."""
         t1 = self.T + 1 if t1 is None else int(t1)
         c1 = min(t1, self.T)
         X = np.empty((t1 - t0, self.D), np.float32)
         Xh = np.empty((max(c1 - t0, 0), self.D), np.float32)
         Eh = np.empty_like(Xh)
         valid = np.empty(max(c1 - t0, 0), np.uint8)
-        _check(self.lib.paraanya_read_state(self.h, int(t0), int(t1), X.ctypes.data_as(C.c_void_p),
+        _check(self.lib.paraanya_read_state_sample(self.h, int(n), int(t0), int(t1), X.ctypes.data_as(C.c_void_p),
                                             Xh.ctypes.data_as(C.c_void_p), Eh.ctypes.data_as(C.c_void_p),
                                             valid.ctypes.data_as(C.c_void_p)))
         return X, Xh, Eh, valid.astype(bool)
 
     def coefficients(self):
+        """(alpha, b, sigma, temb) as the device uses them (temb None for the linear model)."""
         a = np.empty(self.T, np.float64)
         b = np.empty(self.T, np.float64)
+        sg = np.empty(self.T, np.float64)
         temb = np.empty((self.T, self.hidden), np.float32) if self.model == "patch_mlp" else None
         _check(self.lib.paraanya_coefficients(self.h, a.ctypes.data_as(C.c_void_p),
                                               b.ctypes.data_as(C.c_void_p),
+                                              sg.ctypes.data_as(C.c_void_p),
                                               None if temb is None else temb.ctypes.data_as(C.c_void_p)))
-        return a, b, temb
+        return a, b, sg, temb
 
     def kernel_times(self) -> dict:
         kt = KTimes()

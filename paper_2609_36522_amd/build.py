@@ -32,7 +32,7 @@ def hipcc() -> str:
 def command(out: str = LIB) -> list:
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
     return [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-            "-x", "hip", "-Wall", "-fvisibility=hidden", "-Wno-unused-command-line-argument",
+            "-x", "hip", "-Wall", "-Wshadow", "-Werror=shadow", "-fvisibility=hidden", "-Wno-unused-command-line-argument",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
             "-I", INCLUDE, "-I", CSRC, *srcs, "-o", out]
 

@@ -18,7 +18,7 @@ import numpy as np
 from scipy.special import erf, erfc
 
 A_MAX = 5.0
-DEG = 6
+DEG = 7
 
 
 def fit(deg=DEG, amax=A_MAX, iters=60):

@@ -1,8 +1,10 @@
 // Batched evaluation of the cache misses by the patch-MLP noise network, one fused
 // persistent kernel for gfx950 (the single batched forward pass over the misses, Sec. 2.2).
 //
-// Work item = (miss j, block of 128 tokens, half of the hidden-out units of GEMM2). For one
-// item the block
+// Work item = (miss j, block of 128 tokens, half of the hidden-out units of GEMM2). The
+// misses of all samples of a handle form one list (sample-major, each sample's misses in
+// its ascending order); a prefix over the samples' miss counts maps a list entry back to
+// (sample, miss). For one item the block
 //   0. gathers the 128 tokens (2x2 patches, 16 features) of latent x_t, rounds to bf16;
 //   1. h1^T = GELU(W1^T x^T + e_t) in K-chunks of 256 units: MFMA 32x32x16 bf16, K = 16; bf16
 //      result in LDS ([token][unit], padded rows), two chunk buffers of 66 KB;
@@ -45,19 +47,21 @@ constexpr int kFeat = 16;               // 2x2 patch x 4 channels
 constexpr int kXRow = kFeat + 8;        // padded LDS row of the token tile (bf16)
 
 // erf-GELU, x * Phi(x) = max(x, 0) - a Q(a) with a = |x| and Q the normal upper tail,
-// branch-free. Q(a) = 2^(-P(min(a, 5))) with P a degree-6 polynomial fitted toward the
-// minimax relative error of Q (derivation: gelu_fit.py). One v_exp_f32 and seven FMA-class
-// instructions per element; in fp32 the result is within 2.0e-6 max(1, |x|) of the exact
-// erf GELU and within 1.1e-5 (x > 0) / 1.4e-5 (x < 0) relative. Every GELU output is rounded
-// to bf16 next (relative step 2^-8), so a higher degree buys no accuracy that survives.
+// branch-free. Q(a) = 2^(-P(min(a, 5))) with P a degree-7 polynomial fitted toward the
+// minimax relative error of Q (derivation: gelu_fit.py). One v_exp_f32 and eight FMA-class
+// instructions per element; in fp32 the result is within 5.1e-7 max(1, |x|) of the exact
+// erf GELU and within 2.3e-6 (x > 0) / 4.1e-6 (x < 0) relative. Every GELU output is
+// rounded to bf16 next; the residual error is kept near the fp32 accumulation error of the
+// products so that it adds few rounding flips of its own.
 __device__ __forceinline__ float gelu_erf(float x) {
     const float a = fminf(fabsf(x), 5.0f);
-    float p = fmaf(a, -2.945823871414177e-05f, 0.0007087842677719891f);
-    p = fmaf(p, a, -0.007746023125946522f);
-    p = fmaf(p, a, 0.05260632187128067f);
-    p = fmaf(p, a, 0.4596254229545593f);
-    p = fmaf(p, a, 1.150867223739624f);
-    p = fmaf(p, a, 1.0000176429748535f);
+    float p = fmaf(a, 1.601676331119961e-06f, -5.784422319266014e-05f);
+    p = fmaf(p, a, 0.0009071276872418821f);
+    p = fmaf(p, a, -0.008436893112957478f);
+    p = fmaf(p, a, 0.05385196581482887f);
+    p = fmaf(p, a, 0.45854055881500244f);
+    p = fmaf(p, a, 1.1512316465377808f);
+    p = fmaf(p, a, 0.9999960660934448f);
     const float q = __builtin_amdgcn_exp2f(-p);
     return fmaf(-fabsf(x), q, fmaxf(x, 0.0f));
 }
@@ -102,12 +106,24 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     float* red = reinterpret_cast<float*>(&h1s[0][0]);   // [kWaves][kTok][16] after GEMM2
     static_assert(kWaves * kTok * kFeat * 4 <= 2 * kTok * HRow * 2, "reduction buffer must fit");
 
-    const Ctrl* ctrl = d.ctrl;
-    if (ctrl->done) return;
-    const int nblk = d.ntok / kTok;
-    const int items = ctrl->m * nblk * NS;
-    const int newest = ctrl->newest;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    // Misses per sample (0 once a sample is done), inclusive prefix over the samples.
+    __shared__ int mpre[PA_MAX_BATCH + 1];
+    static_assert(PA_MAX_BATCH <= 64, "one wave scans the samples");
+    if (w == 0) {
+        int v = 0;
+        if (lane < d.N) v = d.ctrl[lane].done ? 0 : d.ctrl[lane].m;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int u = __shfl_up(v, off, 64);
+            if (lane >= off) v += u;
+        }
+        if (lane < d.N) mpre[lane + 1] = v;
+        if (lane == 0) mpre[0] = 0;
+    }
+    __syncthreads();
+    const int nblk = d.ntok / kTok;
+    const int items = mpre[d.N] * nblk * NS;
     const int g = lane >> 5, l32 = lane & 31;
     const f32x16 zero16 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
                            0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -116,9 +132,13 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         const int ns = item % NS;
         const int rest = item / NS;
-        const int tb = rest % nblk, jm = rest / nblk;
+        const int tb = rest % nblk, gm = rest / nblk;
+        int n = 0;
+        while (mpre[n + 1] <= gm) ++n;               // sample of list entry gm (uniform)
+        const int jm = gm - mpre[n];
+        const Ctrl* ctrl = d.ctrl + n;
         const int t = ctrl->miss_idx[jm];
-        const float* xt = d.X + (size_t)min(t, newest) * d.D;   // states beyond newest: its copy
+        const float* xt = d.X + ((size_t)n * (d.T + 1) + min(t, ctrl->newest)) * d.D;   // beyond newest: its copy
         const float* et = d.temb + (size_t)t * H;
         const int hb0 = ns * (kNH / 32) + w * 2;   // this wave's first 32-unit block of W2^T
 
@@ -255,7 +275,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         __syncthreads();
 
         // ---- 4. fixed-order sum over waves, unpatchify, store this half's partial output
-        float* out = d.Ep + ((size_t)ns * d.P + jm) * d.D;
+        float* out = d.Ep + (((size_t)ns * d.N + n) * d.P + jm) * d.D;
         for (int e = tid; e < kTok * kFeat; e += NT) {
             const TokPos p = tok_pos(e, tb, d.Himg, d.Wimg);
             float sum = 0.f;

@@ -1,6 +1,8 @@
 // Solver-side kernels of the sampler, for gfx950 (wave64). One sweep is
 //   [k_eps_mlp: network on the misses (patch-MLP only)] -> k_picard -> k_slide
-// and k_reset prepares the first window.
+// and k_reset prepares the first window. Every kernel handles the N samples of a handle
+// at once (grid dimension y of k_reset and k_picard, the blocks of k_slide); a sample that
+// is done makes its blocks exit at once.
 //   k_picard : Eq. (6) assembly (cached output for hits, fresh for misses), Eq. (7) cache
 //              update, DDIM drift at the current latents, the Eq. (1) prefix sum over the
 //              window anchored at its start (blocked scan: register scan per thread, chunk
@@ -54,6 +56,12 @@ __device__ __forceinline__ double4 drift(double alpha, float4 x, double b, float
                         fma(b, (double)e.z, alpha * (double)x.z), fma(b, (double)e.w, alpha * (double)x.w));
 }
 
+// d += sigma * z (the pre-sampled noise term of a stochastic step).
+__device__ __forceinline__ double4 add_noise(double4 d, double sigma, float4 z) {
+    return make_double4(fma(sigma, (double)z.x, d.x), fma(sigma, (double)z.y, d.y),
+                        fma(sigma, (double)z.z, d.z), fma(sigma, (double)z.w, d.w));
+}
+
 __device__ __forceinline__ double abs_dev(float4 a, float4 b) {
     return (fabs((double)a.x - (double)b.x) + fabs((double)a.y - (double)b.y)) +
            (fabs((double)a.z - (double)b.z) + fabs((double)a.w - (double)b.w));
@@ -70,18 +78,21 @@ __device__ __forceinline__ double sq_dev(float4 a, float4 b) {
 // ---------------------------------------------------------------------------- reset
 // Window [0, min(P, T)); no timestep has a cache entry, so every slot is a first-entry miss.
 __global__ void k_reset(Dev d) {
+    const int n = blockIdx.y;
     const int tid = blockIdx.x * blockDim.x + threadIdx.x;
-    Ctrl* c = d.ctrl;
+    Ctrl* c = d.ctrl + n;
+    uint8_t* valid = d.valid + (size_t)n * d.T;
+    pa_sweep_trace_t* tr = d.trace ? d.trace + (size_t)n * d.T : nullptr;
     const int W = min(d.P, d.T);
-    for (int t = tid; t < d.T; t += gridDim.x * blockDim.x) d.valid[t] = 0;
+    for (int t = tid; t < d.T; t += gridDim.x * blockDim.x) valid[t] = 0;
     for (int j = tid; j < W; j += gridDim.x * blockDim.x) {
         c->miss_idx[j] = j;
         c->slot_miss[j] = 1;
         c->slot_rank[j] = (uint8_t)j;
-        if (d.trace) {
-            d.trace[0].dev[j] = __builtin_nan("");
-            d.trace[0].hit[j] = 0;
-            d.trace[0].miss_idx[j] = j;
+        if (tr) {
+            tr[0].dev[j] = __builtin_nan("");
+            tr[0].hit[j] = 0;
+            tr[0].miss_idx[j] = j;
         }
     }
     if (tid == 0) {
@@ -95,10 +106,12 @@ __global__ void k_reset(Dev d) {
         c->sweep = 0;
         c->nfe = W;
         c->hits = 0;
-        if (d.trace) {
-            d.trace[0].s = 0;
-            d.trace[0].e = W;
-            d.trace[0].m = W;
+        c->revisits = 0;
+        c->revisits_below = 0;
+        if (tr) {
+            tr[0].s = 0;
+            tr[0].e = W;
+            tr[0].m = W;
         }
     }
 }
@@ -107,7 +120,7 @@ hipError_t launch_reset(const Dev& d, hipStream_t st) {
     int blocks = (d.T + kThreads - 1) / kThreads;
     if (blocks < 1) blocks = 1;
     if (blocks > 64) blocks = 64;
-    hipLaunchKernelGGL(k_reset, dim3(blocks), dim3(kThreads), 0, st, d);
+    hipLaunchKernelGGL(k_reset, dim3(blocks, d.N), dim3(kThreads), 0, st, d);
     return hipGetLastError();
 }
 
@@ -130,7 +143,8 @@ int picard_blocks(int D) { return (D / 4 + kCols - 1) / kCols; }
 // fixed-order sum of the network kernel's partial outputs.
 template <int TPT, bool LINEAR>
 __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
-    Ctrl* ctrl = d.ctrl;
+    const int n = blockIdx.y;
+    Ctrl* ctrl = d.ctrl + n;
     if (ctrl->done) return;
     const int s = ctrl->s, e = ctrl->e, W = e - s, newest = ctrl->newest;
     const int tid = threadIdx.x;
@@ -140,6 +154,10 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     const bool colok = c4 < n4;
     const int j0 = row * TPT;
     const size_t D = (size_t)d.D;
+    float* X = d.X + (size_t)n * (d.T + 1) * D;
+    float* Xh = d.Xh + (size_t)n * d.T * D;
+    float* Eh = d.Eh + (size_t)n * d.T * D;
+    const float* noise = d.noise ? d.noise + (size_t)n * d.T * D : nullptr;
     const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
     const double4 dzero = make_double4(0.0, 0.0, 0.0, 0.0);
 
@@ -151,7 +169,7 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     for (int k = 0; k <= TPT; ++k) {
         const int j = j0 + k;
         const int t = min(s + j, newest);
-        xs[k] = (j <= W && colok) ? reinterpret_cast<const float4*>(d.X + t * D)[c4] : zero;
+        xs[k] = (j <= W && colok) ? reinterpret_cast<const float4*>(X + t * D)[c4] : zero;
     }
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
@@ -168,26 +186,27 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
                     eps = make_float4(ct * x.x, ct * x.y, ct * x.z, ct * x.w);
                 } else {
                     // Fresh output = fixed-order sum of the network kernel's partials.
-                    const float* ep = d.Ep + (size_t)ctrl->slot_rank[j] * D;
+                    const float* ep = d.Ep + ((size_t)n * d.P + ctrl->slot_rank[j]) * D;
                     eps = reinterpret_cast<const float4*>(ep)[c4];
                     for (int h = 1; h < d.nsplit; ++h) {
-                        const float4 p = reinterpret_cast<const float4*>(ep + (size_t)h * d.P * D)[c4];
+                        const float4 p = reinterpret_cast<const float4*>(ep + (size_t)h * d.N * d.P * D)[c4];
                         eps = make_float4(eps.x + p.x, eps.y + p.y, eps.z + p.z, eps.w + p.w);
                     }
                 }
-                reinterpret_cast<float4*>(d.Eh + t * D)[c4] = eps;   // Eq. (7) output
-                reinterpret_cast<float4*>(d.Xh + t * D)[c4] = x;     // Eq. (7) input
+                reinterpret_cast<float4*>(Eh + t * D)[c4] = eps;   // Eq. (7) output
+                reinterpret_cast<float4*>(Xh + t * D)[c4] = x;     // Eq. (7) input
             } else {
-                eps = reinterpret_cast<const float4*>(d.Eh + t * D)[c4];  // Eq. (6) hit
+                eps = reinterpret_cast<const float4*>(Eh + t * D)[c4];  // Eq. (6) hit
             }
-            dr[k] = drift(d.coef[2 * t], x, d.coef[2 * t + 1], eps);
+            dr[k] = drift(d.coef[3 * t], x, d.coef[3 * t + 1], eps);
+            if (noise) dr[k] = add_noise(dr[k], d.coef[3 * t + 2], reinterpret_cast<const float4*>(noise + t * D)[c4]);
         }
         // Cache entry the updated state s + 1 + j is tested against in the next sweep.
         if (j + 1 < W && colok)
             xhn[k] = ctrl->slot_miss[j + 1] ? xs[k + 1]
-                                            : reinterpret_cast<const float4*>(d.Xh + (s + 1 + j) * D)[c4];
+                                            : reinterpret_cast<const float4*>(Xh + (s + 1 + j) * D)[c4];
     }
-    if (colok) anchor = reinterpret_cast<const float4*>(d.X + min(s, newest) * D)[c4];
+    if (colok) anchor = reinterpret_cast<const float4*>(X + min(s, newest) * D)[c4];
 
 #pragma unroll
     for (int k = 1; k < TPT; ++k) dr[k] = d4_add(dr[k], dr[k - 1]);
@@ -209,7 +228,7 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
         const float4 y = make_float4((float)yd.x, (float)yd.y, (float)yd.z, (float)yd.w);
         double rs = 0.0, ds = 0.0;
         if (colok) {
-            reinterpret_cast<float4*>(d.X + (s + 1 + j) * D)[c4] = y;
+            reinterpret_cast<float4*>(X + (s + 1 + j) * D)[c4] = y;
             rs = sq_dev(y, xs[k + 1]);                   // Eq. (2) vs the previous iterate
             if (j + 1 < W) ds = abs_dev(y, xhn[k]);      // Eq. (4) for the next sweep
         }
@@ -223,15 +242,16 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     __syncthreads();
     const int nblk = gridDim.x;
     if (tid < W) {
-        d.part_res[tid * nblk + blockIdx.x] = rres[tid];
-        d.part_dev[tid * nblk + blockIdx.x] = rdev[tid];
-        if (blockIdx.x == 0 && ctrl->slot_miss[tid]) d.valid[s + tid] = 1;   // Eq. (7) entry
+        const size_t pbase = (size_t)n * d.P * nblk;
+        d.part_res[pbase + tid * nblk + blockIdx.x] = rres[tid];
+        d.part_dev[pbase + tid * nblk + blockIdx.x] = rdev[tid];
+        if (blockIdx.x == 0 && ctrl->slot_miss[tid]) d.valid[(size_t)n * d.T + s + tid] = 1;   // Eq. (7) entry
     }
 }
 
 template <bool LINEAR>
 static hipError_t launch_picard_t(const Dev& d, hipStream_t st) {
-    const dim3 grid(d.picard_blocks), block(kThreads);
+    const dim3 grid(d.picard_blocks, d.N), block(kThreads);
     switch (picard_tpt(d.P)) {
         case 1: hipLaunchKernelGGL((k_picard<1, LINEAR>), grid, block, 0, st, d); break;
         case 2: hipLaunchKernelGGL((k_picard<2, LINEAR>), grid, block, 0, st, d); break;
@@ -254,8 +274,10 @@ hipError_t launch_picard(const Dev& d, hipStream_t st, int linear) {
 // over s+1..e-1, the slide s' = s + 1 + c, done; then the next window's hit test and
 // compaction. Every barrier below is reached by all threads of the block.
 __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
-    Ctrl* ctrl = d.ctrl;
+    const int n = blockIdx.x;
+    Ctrl* ctrl = d.ctrl + n;
     if (ctrl->done) return;
+    pa_sweep_trace_t* const trace = d.trace ? d.trace + (size_t)n * d.T : nullptr;
     const int s = ctrl->s, e = ctrl->e, W = e - s;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int nblk = d.picard_blocks;
@@ -265,6 +287,8 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
     __shared__ int wfirst[4];
     __shared__ int wbad[4];
     __shared__ int wcount[4];
+    __shared__ int wrev[4];
+    __shared__ int wbelow[4];
     __shared__ int s_next;
 
     const int NQ = 2 * W;                   // q < W: residual q; q >= W: deviation q - W
@@ -274,7 +298,9 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
         const int q = tid / G, sub = tid - q * G;
         double acc = 0.0;
         if (q < NQ) {
-            const double* pr = (q < W) ? d.part_res + (size_t)q * nblk : d.part_dev + (size_t)(q - W) * nblk;
+            const size_t pbase = (size_t)n * d.P * nblk;
+            const double* pr = (q < W) ? d.part_res + pbase + (size_t)q * nblk
+                                       : d.part_dev + pbase + (size_t)(q - W) * nblk;
 #pragma unroll 16
             for (int b = sub; b < nblk; b += G) acc += pr[b];
         }
@@ -301,7 +327,7 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
             wfirst[wave] = sm ? wave * 64 + __ffsll((long long)sm) - 1 : 1 << 30;
             wbad[wave] = bm != 0ull;
         }
-        if (d.trace && j < W) d.trace[ctrl->sweep].resid[j] = r;
+        if (trace && j < W) trace[ctrl->sweep].resid[j] = r;
     }
     __syncthreads();
     if (tid == 0) {
@@ -312,8 +338,8 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
         }
         const int s2 = s + 1 + c;
         if (anybad) ctrl->nonfinite = 1;
-        if (d.trace) {
-            pa_sweep_trace_t* rec = d.trace + ctrl->sweep;
+        if (trace) {
+            pa_sweep_trace_t* rec = trace + ctrl->sweep;
             rec->c = c;
             rec->s_next = s2;
             rec->sweep = ctrl->sweep;
@@ -329,7 +355,7 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
         // host only reads this word and synchronizes the stream before reading anything else).
         const uint64_t word = ((uint64_t)(uint32_t)ctrl->sweep << 32) |
                               ((uint64_t)(s2 >= d.T) << 31) | (uint64_t)(uint32_t)min(s2, d.T);
-        __hip_atomic_store(d.progress, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(d.progress + n, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
     __syncthreads();
     const int s2 = s_next;
@@ -341,17 +367,25 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
     const int next = ctrl->sweep;           // index of the next sweep (set above by tid 0)
     const int j = tid, t = s2 + j;
     double dev = __builtin_nan("");
-    bool hit = false, miss = false;
+    bool hit = false, miss = false, rev = false, below = false;
     if (j < W2) {
         if (t < e) {
             dev = dv_s[t - s - 1];
             hit = dev < d.delta;            // strict: delta == 0 never hits
+            rev = true;                     // t holds a cache entry: a revisit
+            below = dev < d.revisit_thr;
         }
         miss = !hit;
     }
     const unsigned long long mask = __ballot(miss);
+    const unsigned long long rmask = __ballot(rev);
+    const unsigned long long bmask = __ballot(below);
     const int rank = __popcll(mask & lanemask_lt());
-    if (wave < 4 && lane == 0) wcount[wave] = __popcll(mask);
+    if (wave < 4 && lane == 0) {
+        wcount[wave] = __popcll(mask);
+        wrev[wave] = __popcll(rmask);
+        wbelow[wave] = __popcll(bmask);
+    }
     __syncthreads();
     if (j < 256) {
         int off = 0;
@@ -362,8 +396,8 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
             ctrl->slot_miss[j] = miss ? 1 : 0;
             ctrl->slot_rank[j] = miss ? (uint8_t)(off + rank) : 0;
         }
-        if (d.trace) {
-            pa_sweep_trace_t* rec = d.trace + next;
+        if (trace) {
+            pa_sweep_trace_t* rec = trace + next;
             if (j < W2) {
                 rec->dev[j] = dev;
                 rec->hit[j] = hit ? 1 : 0;
@@ -379,12 +413,14 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
             ctrl->m = m;
             ctrl->nfe += m;
             ctrl->hits += W2 - m;
+            ctrl->revisits += wrev[0] + wrev[1] + wrev[2] + wrev[3];
+            ctrl->revisits_below += wbelow[0] + wbelow[1] + wbelow[2] + wbelow[3];
         }
     }
 }
 
 hipError_t launch_slide(const Dev& d, hipStream_t st) {
-    hipLaunchKernelGGL(k_slide, dim3(1), dim3(kSlideThreads), 0, st, d);
+    hipLaunchKernelGGL(k_slide, dim3(d.N), dim3(kSlideThreads), 0, st, d);
     return hipGetLastError();
 }
 

@@ -8,7 +8,7 @@
 
 namespace pa {
 
-// Device-resident control block of one handle. Every per-sweep decision lives here, so
+// Device-resident control block of one sample. Every per-sweep decision lives here, so
 // the host can enqueue sweeps without reading anything back.
 struct alignas(256) Ctrl {
     int32_t s;          // window start: states 0..s are final
@@ -21,35 +21,40 @@ struct alignas(256) Ctrl {
     int32_t sweep;      // completed sweeps since reset
     int64_t nfe;
     int64_t hits;
-    int32_t pad[4];
+    int64_t revisits;       // window slots whose timestep holds a cache entry
+    int64_t revisits_below; // ... with Eq. (4) deviation below Dev::revisit_thr
     int32_t miss_idx[PA_MAX_WINDOW];  // ascending miss timesteps
     uint8_t slot_miss[PA_MAX_WINDOW]; // per window slot j: 1 if t = s + j is a miss
     uint8_t slot_rank[PA_MAX_WINDOW]; // per miss slot j: its position in miss_idx
 };
 
-// Geometry and device buffers handed to every kernel launcher.
+// Geometry and device buffers handed to every kernel launcher. Per-sample buffers are
+// stacked along a leading sample index n < N.
 struct Dev {
+    int32_t N;                 // samples
     int32_t T, P, D;
     int32_t C, Himg, Wimg;
     int32_t ntok, hidden;      // patch-MLP only
     double delta, tol;
-    float* X;                  // [T+1][D] trajectory
-    float* Xh;                 // [T][D]   cached inputs
-    float* Eh;                 // [T][D]   cached outputs
-    uint8_t* valid;            // [T]
-    double* coef;              // [T][2]   (alpha_i, b_i) in fp64
-    float* lin_c;              // [T]      linear network coefficients (or null)
-    double* part_res;          // [P][picard_blocks] fp64 partial sums of Eq. (2) residuals
-    double* part_dev;          // [P][picard_blocks] fp64 partial sums of Eq. (4) deviations
-    Ctrl* ctrl;
-    uint64_t* progress;        // host-mapped word: completed sweeps << 32 | done << 31 | s
-    pa_sweep_trace_t* trace;   // [T] or null
+    double revisit_thr;        // threshold of the revisit counters
+    float* X;                  // [N][T+1][D] trajectories
+    float* Xh;                 // [N][T][D]   cached inputs
+    float* Eh;                 // [N][T][D]   cached outputs
+    uint8_t* valid;            // [N][T]
+    const float* noise;        // [N][T][D]   pre-sampled step noise z (eta > 0), else null
+    double* coef;              // [T][3]      (alpha_i, b_i, sigma_i) in fp64
+    float* lin_c;              // [T]         linear network coefficients (or null)
+    double* part_res;          // [N][P][picard_blocks] fp64 partial sums of Eq. (2) residuals
+    double* part_dev;          // [N][P][picard_blocks] fp64 partial sums of Eq. (4) deviations
+    Ctrl* ctrl;                // [N]
+    uint64_t* progress;        // [N] host-mapped words: sweeps << 32 | done << 31 | s
+    pa_sweep_trace_t* trace;   // [N][T] or null
     // patch-MLP weights in device layouts
     const __bf16* w1t;         // [hidden][16]     (transposed W1)
     const __bf16* w2f;         // W2^T fragment-major: [hidden/32][hidden/16][64 lanes][8]
     const __bf16* w3p;         // [hidden/32][2][64][8] lane-permuted W3 fragments
     float* temb;               // [T][hidden]      e_j = temb(t_j) Wt
-    float* Ep;                 // [nsplit][P][D]   per-half network outputs of the misses
+    float* Ep;                 // [nsplit][N][P][D] per-half network outputs of the misses
     int32_t nsplit;            // halves of the output units (partials summed by k_picard)
     int32_t picard_blocks;
     int32_t mlp_grid;

@@ -50,9 +50,11 @@ struct paraanya {
     uint32_t flags = 0;
     int model = PA_EPS_LINEAR;
     int temb_dim = 0;
-    std::vector<double> coef_host;    // [T][2] as uploaded
-    Ctrl* ctrl_host = nullptr;        // pinned mirror
-    uint64_t* progress_host = nullptr; // pinned, device-mapped progress word (see k_slide)
+    std::vector<double> coef_host;    // [T][3] as uploaded
+    Ctrl* ctrl_host = nullptr;        // pinned mirror, one block per sample
+    uint64_t* progress_host = nullptr; // pinned, device-mapped progress words (see k_slide)
+    float* noise_buf = nullptr;       // [N][T][D] step noise (eta > 0)
+    bool noise_set = false;
     bool ctrl_fresh = false;           // ctrl_host matches the device and nothing is queued
     bool have_reset = false;
     bool host_done = false;           // done flag of the last synchronized read
@@ -88,11 +90,18 @@ struct paraanya {
     int read_ctrl() {
         // The mirror stays valid until the next enqueue, so repeated queries cost nothing.
         if (ctrl_fresh) return PA_OK;
-        PA_HIP(hipMemcpyAsync(ctrl_host, d.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, stream));
+        PA_HIP(hipMemcpyAsync(ctrl_host, d.ctrl, (size_t)d.N * sizeof(Ctrl), hipMemcpyDeviceToHost, stream));
         PA_HIP(hipStreamSynchronize(stream));
-        host_done = ctrl_host->done != 0;
+        host_done = true;
+        for (int n = 0; n < d.N; ++n) host_done = host_done && ctrl_host[n].done != 0;
         ctrl_fresh = true;
         return PA_OK;
+    }
+
+    bool any_nonfinite() const {
+        for (int n = 0; n < d.N; ++n)
+            if (ctrl_host[n].nonfinite) return true;
+        return false;
     }
 
     int drain_profile() {
@@ -177,6 +186,7 @@ int build_schedule(const pa_schedule_t* sc, int T, std::vector<double>& ab, std:
     } else {
         return fail(PA_ERR_INVALID_ARG, "schedule: unknown kind %d", sc->kind);
     }
+    if (!(sc->eta >= 0.0 && sc->eta <= 1.0)) return fail(PA_ERR_INVALID_ARG, "schedule: eta must lie in [0, 1] (got %g)", sc->eta);
     return PA_OK;
 }
 
@@ -208,7 +218,7 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     // ---- validation: no HIP call before this block completes
     if (!latent_shape || !schedule || !eps_model) return fail(PA_ERR_INVALID_ARG, "NULL argument");
     const int N = latent_shape[0], C = latent_shape[1], Hi = latent_shape[2], Wi = latent_shape[3];
-    if (N != 1) return fail(PA_ERR_INVALID_ARG, "batch N must be 1 (got %d)", N);
+    if (N < 1 || N > PA_MAX_BATCH) return fail(PA_ERR_INVALID_ARG, "batch N must be in [1, %d] (got %d)", PA_MAX_BATCH, N);
     if (C < 1 || Hi < 1 || Wi < 1) return fail(PA_ERR_INVALID_ARG, "latent dims must be positive");
     const long long Dl = (long long)C * Hi * Wi;
     if (Dl % 4 != 0) return fail(PA_ERR_INVALID_ARG, "C*H*W must be a multiple of 4");
@@ -238,12 +248,16 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     std::vector<double> ab, tv;
     int rc = build_schedule(schedule, T, ab, tv);
     if (rc) return rc;
-    // DDIM one-step increment d_i = alpha_i x_i + b_i eps_i (eta = 0), fp64.
-    std::vector<double> coef(2 * (size_t)T);
+    // One-step increment d_i = alpha_i x_i + b_i eps_i + sigma_i z_i of the generalized DDIM
+    // step with eta (eta = 0: DDIM; eta = 1: ancestral DDPM), fp64.
+    const double eta = schedule->eta;
+    std::vector<double> coef(3 * (size_t)T);
     for (int i = 0; i < T; ++i) {
         const double a = sqrt(ab[i + 1] / ab[i]);
-        coef[2 * i] = a - 1.0;
-        coef[2 * i + 1] = sqrt(1.0 - ab[i + 1]) - a * sqrt(1.0 - ab[i]);
+        const double sig = eta * sqrt((1.0 - ab[i + 1]) / (1.0 - ab[i])) * sqrt(1.0 - ab[i] / ab[i + 1]);
+        coef[3 * i] = a - 1.0;
+        coef[3 * i + 1] = sqrt(1.0 - ab[i + 1] - sig * sig) - a * sqrt(1.0 - ab[i]);
+        coef[3 * i + 2] = sig;
     }
     if (em->kind == PA_EPS_LINEAR)
         for (int j = 0; j < T; ++j)
@@ -257,8 +271,9 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     h->model = em->kind;
     h->coef_host = coef;
     Dev& d = h->d;
-    d.T = T; d.P = window; d.D = D; d.C = C; d.Himg = Hi; d.Wimg = Wi;
+    d.N = N; d.T = T; d.P = window; d.D = D; d.C = C; d.Himg = Hi; d.Wimg = Wi;
     d.delta = delta; d.tol = tol;
+    d.revisit_thr = 0.05;
     d.picard_blocks = pa::picard_blocks(D);
     auto bail = [&](int code) { delete h; return code; };
 
@@ -270,22 +285,28 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     if (he != hipSuccess) return bail(hip_fail(he, "hipDeviceGetAttribute"));
 
     const size_t Dz = (size_t)D;
-    if ((rc = h->alloc(&d.X, (size_t)(T + 1) * Dz, "X"))) return bail(rc);
-    if ((rc = h->alloc(&d.Xh, (size_t)T * Dz, "Xh"))) return bail(rc);
-    if ((rc = h->alloc(&d.Eh, (size_t)T * Dz, "Eh"))) return bail(rc);
-    if ((rc = h->alloc(&d.valid, (size_t)T, "valid"))) return bail(rc);
-    if ((rc = h->alloc(&d.coef, 2 * (size_t)T, "coef"))) return bail(rc);
-    if ((rc = h->alloc(&d.part_res, (size_t)window * d.picard_blocks, "part_res"))) return bail(rc);
-    if ((rc = h->alloc(&d.part_dev, (size_t)window * d.picard_blocks, "part_dev"))) return bail(rc);
-    if ((rc = h->alloc(&d.ctrl, 1, "ctrl"))) return bail(rc);
+    const size_t Nz = (size_t)N;
+    if ((rc = h->alloc(&d.X, Nz * (T + 1) * Dz, "X"))) return bail(rc);
+    if ((rc = h->alloc(&d.Xh, Nz * T * Dz, "Xh"))) return bail(rc);
+    if ((rc = h->alloc(&d.Eh, Nz * T * Dz, "Eh"))) return bail(rc);
+    if ((rc = h->alloc(&d.valid, Nz * T, "valid"))) return bail(rc);
+    if ((rc = h->alloc(&d.coef, 3 * (size_t)T, "coef"))) return bail(rc);
+    if ((rc = h->alloc(&d.part_res, Nz * window * d.picard_blocks, "part_res"))) return bail(rc);
+    if ((rc = h->alloc(&d.part_dev, Nz * window * d.picard_blocks, "part_dev"))) return bail(rc);
+    if ((rc = h->alloc(&d.ctrl, Nz, "ctrl"))) return bail(rc);
     if (flags & PA_FLAG_TRACE)
-        if ((rc = h->alloc(&d.trace, (size_t)T, "trace"))) return bail(rc);
-    he = hipHostMalloc((void**)&h->ctrl_host, sizeof(Ctrl), hipHostMallocDefault);
+        if ((rc = h->alloc(&d.trace, Nz * T, "trace"))) return bail(rc);
+    if (eta > 0.0) {
+        if ((rc = h->alloc(&h->noise_buf, Nz * T * Dz, "noise"))) return bail(rc);
+        d.noise = h->noise_buf;
+    }
+    he = hipHostMalloc((void**)&h->ctrl_host, Nz * sizeof(Ctrl), hipHostMallocDefault);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostMalloc"));
-    memset(h->ctrl_host, 0, sizeof(Ctrl));
-    he = hipHostMalloc((void**)&h->progress_host, 256, hipHostMallocMapped | hipHostMallocCoherent);
+    memset(h->ctrl_host, 0, Nz * sizeof(Ctrl));
+    he = hipHostMalloc((void**)&h->progress_host, Nz * sizeof(uint64_t) < 256 ? 256 : Nz * sizeof(uint64_t),
+                       hipHostMallocMapped | hipHostMallocCoherent);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostMalloc(progress)"));
-    *h->progress_host = 0;
+    for (int n = 0; n < N; ++n) h->progress_host[n] = 0;
     he = hipHostGetDevicePointer((void**)&d.progress, h->progress_host, 0);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostGetDevicePointer"));
 
@@ -338,7 +359,7 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
         if ((rc = h->alloc(&tvd, (size_t)T, "t_values"))) return bail(rc);
         if ((rc = h->alloc(&d.temb, (size_t)T * Hd, "temb"))) return bail(rc);
         d.nsplit = pa::mlp_splits(Hd);
-        if ((rc = h->alloc(&d.Ep, (size_t)d.nsplit * window * Dz, "Ep"))) return bail(rc);
+        if ((rc = h->alloc(&d.Ep, (size_t)d.nsplit * Nz * window * Dz, "Ep"))) return bail(rc);
         PA_HIP_BAIL(hipMemcpyAsync(w1d, w1t.data(), w1t.size() * 2, hipMemcpyHostToDevice, h->stream));
         PA_HIP_BAIL(hipMemcpyAsync(w2d, w2f.data(), w2f.size() * 2, hipMemcpyHostToDevice, h->stream));
         PA_HIP_BAIL(hipMemcpyAsync(w3d, w3p.data(), w3p.size() * 2, hipMemcpyHostToDevice, h->stream));
@@ -358,17 +379,38 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
 int paraanya_reset(paraanya_t* h, const float* x_init) {
     g_err.clear();
     if (!h || !x_init) return fail(PA_ERR_INVALID_ARG, "NULL argument");
+    if (h->noise_buf && !h->noise_set) return fail(PA_ERR_STATE, "eta > 0: set the step noise first (paraanya_set_noise)");
     // No kernel of this handle may still publish progress from an earlier sample.
     PA_HIP(hipStreamSynchronize(h->stream));
-    *h->progress_host = 0;
+    for (int n = 0; n < h->d.N; ++n) h->progress_host[n] = 0;
     h->ctrl_fresh = false;
-    PA_HIP(hipMemcpyAsync(h->d.X, x_init, (size_t)h->d.D * sizeof(float), hipMemcpyDeviceToDevice, h->stream));
+    const size_t row = (size_t)h->d.D * sizeof(float);
+    PA_HIP(hipMemcpy2DAsync(h->d.X, (size_t)(h->d.T + 1) * row, x_init, row, row, (size_t)h->d.N,
+                            hipMemcpyDeviceToDevice, h->stream));
     PA_HIP(pa::launch_reset(h->d, h->stream));
     h->have_reset = true;
     h->host_done = false;
     h->ev_used = 0;
     h->prof_ms = 0.0;
     h->prof_launches = 0;
+    return PA_OK;
+}
+
+int paraanya_set_noise(paraanya_t* h, const float* z) {
+    g_err.clear();
+    if (!h || !z) return fail(PA_ERR_INVALID_ARG, "NULL argument");
+    if (!h->noise_buf) return fail(PA_ERR_INVALID_ARG, "handle has eta = 0: no step noise");
+    PA_HIP(hipMemcpyAsync(h->noise_buf, z, (size_t)h->d.N * h->d.T * h->d.D * sizeof(float),
+                          hipMemcpyDeviceToDevice, h->stream));
+    h->noise_set = true;
+    return PA_OK;
+}
+
+int paraanya_set_revisit_threshold(paraanya_t* h, double threshold) {
+    g_err.clear();
+    if (!h) return fail(PA_ERR_INVALID_ARG, "NULL handle");
+    if (!(threshold >= 0.0)) return fail(PA_ERR_INVALID_ARG, "threshold must be >= 0 (got %g)", threshold);
+    h->d.revisit_thr = threshold;
     return PA_OK;
 }
 
@@ -381,8 +423,8 @@ int paraanya_sweep(paraanya_t* h, int32_t* done) {
     if (rc) return rc;
     if (done) {
         if ((rc = h->read_ctrl())) return rc;
-        *done = h->ctrl_host->done;
-        if (h->ctrl_host->nonfinite) return fail(PA_ERR_NONFINITE, "non-finite residual in sweep %d", h->ctrl_host->sweep - 1);
+        *done = h->host_done ? 1 : 0;
+        if (h->any_nonfinite()) return fail(PA_ERR_NONFINITE, "non-finite residual");
     }
     return PA_OK;
 }
@@ -392,56 +434,67 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
     if (!h || !x_init || !x_out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
     int rc = paraanya_reset(h, x_init);
     if (rc) return rc;
-    const int T = h->d.T, P = h->d.P;
+    const int T = h->d.T, P = h->d.P, N = h->d.N;
     // Launch loop without per-sweep synchronisation: k_slide publishes (completed sweeps,
-    // done, s) to a pinned host word after every sweep; the host keeps enough sweeps in
-    // flight -- at least the kLookahead next ones and at least the ceil((T - s)/P) that are
-    // certainly still needed (s advances by at most P per sweep) -- and stops enqueuing once
-    // done is seen. Sweeps enqueued after done exit at their first instruction. Every sweep
-    // advances s by at least 1, so at most T sweeps are ever enqueued. The stream is polled
-    // while waiting, so a failed or idle stream ends the loop.
+    // done, s) of every sample to a pinned host word after each sweep; the host keeps enough
+    // sweeps in flight -- at least the kLookahead next ones and at least the ceil((T - s)/P)
+    // that the slowest sample certainly still needs (s advances by at most P per sweep) --
+    // and stops enqueuing once every sample is done. Sweeps enqueued after that exit at
+    // their first instruction. Every sweep advances each unfinished sample's s by at least 1,
+    // so at most T sweeps are ever enqueued. The stream is polled while waiting, so a failed
+    // or idle stream ends the loop.
     constexpr int kLookahead = 2;
     volatile uint64_t* prog = h->progress_host;
+    auto scan = [&](int* completed, int* need) {      // returns true once all are done
+        bool all = true;
+        *completed = 0;
+        *need = 0;
+        for (int n = 0; n < N; ++n) {
+            const uint64_t w = prog[n];
+            const int c = (int)(w >> 32), s_now = (int)(w & 0x7fffffffu);
+            if (c > *completed) *completed = c;
+            if ((w >> 31) & 1u) continue;
+            all = false;
+            const int q = (T - s_now + P - 1) / P;
+            if (q > *need) *need = q;
+        }
+        return all;
+    };
     int enqueued = 0;
     for (unsigned spin = 0;; ++spin) {
-        const uint64_t w = *prog;
-        const int completed = (int)(w >> 32), s_now = (int)(w & 0x7fffffffu);
-        if ((w >> 31) & 1u) break;
-        const int need = (T - s_now + P - 1) / P;
+        int completed, need;
+        if (scan(&completed, &need)) break;
         const int want = completed + (need > kLookahead ? need : kLookahead);
         if (enqueued < want && enqueued < T) {
-            const int n = (want < T ? want : T) - enqueued;
-            for (int i = 0; i < n; ++i)
+            const int k = (want < T ? want : T) - enqueued;
+            for (int i = 0; i < k; ++i)
                 if ((rc = h->enqueue_sweep())) return rc;
-            enqueued += n;
+            enqueued += k;
             continue;
         }
         if (spin % 256 != 255) continue;        // poll the stream now and then, not per spin
         const hipError_t q = hipStreamQuery(h->stream);
         if (q == hipSuccess) {
-            // Stream idle: the word is final for the enqueued work.
-            if ((*prog >> 31) & 1u) break;
+            // Stream idle: the words are final for the enqueued work.
+            if (scan(&completed, &need)) break;
             if (enqueued >= T) return fail(PA_ERR_HIP, "sampler did not finish within T sweeps");
         } else if (q != hipErrorNotReady) {
             return hip_fail(q, "hipStreamQuery");
         }
     }
     // One synchronization for the output copy and the counters.
-    PA_HIP(hipMemcpyAsync(x_out, h->d.X + (size_t)T * h->d.D, (size_t)h->d.D * sizeof(float),
-                          hipMemcpyDeviceToDevice, h->stream));
+    const size_t row = (size_t)h->d.D * sizeof(float);
+    PA_HIP(hipMemcpy2DAsync(x_out, row, h->d.X + (size_t)T * h->d.D, (size_t)(T + 1) * row, row,
+                            (size_t)N, hipMemcpyDeviceToDevice, h->stream));
     h->ctrl_fresh = false;
     if ((rc = h->read_ctrl())) return rc;
-    if (h->ctrl_host->nonfinite) return fail(PA_ERR_NONFINITE, "non-finite residual during sampling");
+    if (h->any_nonfinite()) return fail(PA_ERR_NONFINITE, "non-finite residual during sampling");
     return PA_OK;
 }
 
-int paraanya_stats(paraanya_t* h, pa_stats_t* out) {
-    g_err.clear();
-    if (!h || !out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
-    if (!h->have_reset) return fail(PA_ERR_STATE, "stats before reset");
-    int rc = h->read_ctrl();
-    if (rc) return rc;
-    const Ctrl& c = *h->ctrl_host;
+namespace {
+
+void fill_stats(const Ctrl& c, pa_stats_t* out) {
     out->nfe = c.nfe;
     out->hits = c.hits;
     out->misses = c.nfe;
@@ -450,46 +503,100 @@ int paraanya_stats(paraanya_t* h, pa_stats_t* out) {
     out->window_end = c.e;
     out->done = c.done;
     out->nonfinite = c.nonfinite;
+    out->revisits = c.revisits;
+    out->revisits_below = c.revisits_below;
+}
+
+}  // namespace
+
+int paraanya_stats(paraanya_t* h, pa_stats_t* out) {
+    g_err.clear();
+    if (!h || !out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
+    if (!h->have_reset) return fail(PA_ERR_STATE, "stats before reset");
+    int rc = h->read_ctrl();
+    if (rc) return rc;
+    fill_stats(h->ctrl_host[0], out);
+    for (int n = 1; n < h->d.N; ++n) {
+        pa_stats_t o;
+        fill_stats(h->ctrl_host[n], &o);
+        out->nfe += o.nfe;
+        out->hits += o.hits;
+        out->misses += o.misses;
+        out->revisits += o.revisits;
+        out->revisits_below += o.revisits_below;
+        if (o.sweeps > out->sweeps) out->sweeps = o.sweeps;
+        if (o.window_start < out->window_start) out->window_start = o.window_start;
+        if (o.window_end < out->window_end) out->window_end = o.window_end;
+        out->done = out->done && o.done;
+        out->nonfinite = out->nonfinite || o.nonfinite;
+    }
+    return PA_OK;
+}
+
+int paraanya_stats_sample(paraanya_t* h, int32_t n, pa_stats_t* out) {
+    g_err.clear();
+    if (!h || !out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
+    if (n < 0 || n >= h->d.N) return fail(PA_ERR_INVALID_ARG, "sample %d outside [0, %d)", n, h->d.N);
+    if (!h->have_reset) return fail(PA_ERR_STATE, "stats before reset");
+    int rc = h->read_ctrl();
+    if (rc) return rc;
+    fill_stats(h->ctrl_host[n], out);
+    return PA_OK;
+}
+
+int paraanya_trace_sample(paraanya_t* h, int32_t n, int32_t k, pa_sweep_trace_t* out) {
+    g_err.clear();
+    if (!h || !out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
+    if (!(h->flags & PA_FLAG_TRACE)) return fail(PA_ERR_STATE, "handle created without PA_FLAG_TRACE");
+    if (n < 0 || n >= h->d.N) return fail(PA_ERR_INVALID_ARG, "sample %d outside [0, %d)", n, h->d.N);
+    if (!h->have_reset) return fail(PA_ERR_STATE, "trace before reset");
+    int rc = h->read_ctrl();
+    if (rc) return rc;
+    if (k < 0 || k >= h->ctrl_host[n].sweep) return fail(PA_ERR_INVALID_ARG, "sweep %d not completed", k);
+    PA_HIP(hipMemcpy(out, h->d.trace + (size_t)n * h->d.T + k, sizeof(pa_sweep_trace_t), hipMemcpyDeviceToHost));
     return PA_OK;
 }
 
 int paraanya_trace(paraanya_t* h, int32_t k, pa_sweep_trace_t* out) {
+    return paraanya_trace_sample(h, 0, k, out);
+}
+
+int paraanya_read_state_sample(paraanya_t* h, int32_t n, int32_t t0, int32_t t1, float* X, float* Xh,
+                               float* Eh, uint8_t* valid) {
     g_err.clear();
-    if (!h || !out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
-    if (!(h->flags & PA_FLAG_TRACE)) return fail(PA_ERR_STATE, "handle created without PA_FLAG_TRACE");
-    if (!h->have_reset) return fail(PA_ERR_STATE, "trace before reset");
-    int rc = h->read_ctrl();
-    if (rc) return rc;
-    if (k < 0 || k >= h->ctrl_host->sweep) return fail(PA_ERR_INVALID_ARG, "sweep %d not completed", k);
-    PA_HIP(hipMemcpy(out, h->d.trace + k, sizeof(pa_sweep_trace_t), hipMemcpyDeviceToHost));
+    if (!h) return fail(PA_ERR_INVALID_ARG, "NULL handle");
+    const int T = h->d.T;
+    if (n < 0 || n >= h->d.N) return fail(PA_ERR_INVALID_ARG, "sample %d outside [0, %d)", n, h->d.N);
+    if (t0 < 0 || t1 < t0 || t1 > T + 1) return fail(PA_ERR_INVALID_ARG, "row range [%d, %d) invalid", t0, t1);
+    PA_HIP(hipStreamSynchronize(h->stream));
+    const size_t D = (size_t)h->d.D;
+    const float* Xs = h->d.X + (size_t)n * (T + 1) * D;
+    const float* Xhs = h->d.Xh + (size_t)n * T * D;
+    const float* Ehs = h->d.Eh + (size_t)n * T * D;
+    const uint8_t* vs = h->d.valid + (size_t)n * T;
+    const int c1 = t1 < T ? t1 : T;
+    if (X && t1 > t0) PA_HIP(hipMemcpy(X, Xs + t0 * D, (size_t)(t1 - t0) * D * 4, hipMemcpyDeviceToHost));
+    if (c1 > t0) {
+        if (Xh) PA_HIP(hipMemcpy(Xh, Xhs + t0 * D, (size_t)(c1 - t0) * D * 4, hipMemcpyDeviceToHost));
+        if (Eh) PA_HIP(hipMemcpy(Eh, Ehs + t0 * D, (size_t)(c1 - t0) * D * 4, hipMemcpyDeviceToHost));
+        if (valid) PA_HIP(hipMemcpy(valid, vs + t0, (size_t)(c1 - t0), hipMemcpyDeviceToHost));
+    }
     return PA_OK;
 }
 
 int paraanya_read_state(paraanya_t* h, int32_t t0, int32_t t1, float* X, float* Xh, float* Eh,
                         uint8_t* valid) {
-    g_err.clear();
-    if (!h) return fail(PA_ERR_INVALID_ARG, "NULL handle");
-    const int T = h->d.T;
-    if (t0 < 0 || t1 < t0 || t1 > T + 1) return fail(PA_ERR_INVALID_ARG, "row range [%d, %d) invalid", t0, t1);
-    PA_HIP(hipStreamSynchronize(h->stream));
-    const size_t D = (size_t)h->d.D;
-    const int c1 = t1 < T ? t1 : T;
-    if (X && t1 > t0) PA_HIP(hipMemcpy(X, h->d.X + t0 * D, (size_t)(t1 - t0) * D * 4, hipMemcpyDeviceToHost));
-    if (c1 > t0) {
-        if (Xh) PA_HIP(hipMemcpy(Xh, h->d.Xh + t0 * D, (size_t)(c1 - t0) * D * 4, hipMemcpyDeviceToHost));
-        if (Eh) PA_HIP(hipMemcpy(Eh, h->d.Eh + t0 * D, (size_t)(c1 - t0) * D * 4, hipMemcpyDeviceToHost));
-        if (valid) PA_HIP(hipMemcpy(valid, h->d.valid + t0, (size_t)(c1 - t0), hipMemcpyDeviceToHost));
-    }
-    return PA_OK;
+    return paraanya_read_state_sample(h, 0, t0, t1, X, Xh, Eh, valid);
 }
 
-int paraanya_coefficients(paraanya_t* h, double* alpha, double* b, float* temb) {
+int paraanya_coefficients(paraanya_t* h, double* alpha, double* b, double* sigma, float* temb) {
     g_err.clear();
     if (!h) return fail(PA_ERR_INVALID_ARG, "NULL handle");
     const int T = h->d.T;
     for (int i = 0; i < T; ++i) {
-        if (alpha) alpha[i] = h->coef_host[2 * i];
-        if (b) b[i] = h->coef_host[2 * i + 1];
+        if (alpha) alpha[i] = h->coef_host[3 * i];
+        if (b) b[i] = h->coef_host[3 * i + 1];
+        if (sigma) sigma[i] = h->coef_host[3 * i + 2];
     }
     if (temb) {
         if (h->model != PA_EPS_PATCH_MLP) return fail(PA_ERR_INVALID_ARG, "temb requested for a linear model");
@@ -510,7 +617,8 @@ int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out) {
     if (rc) return rc;
     out->launches = h->prof_launches;
     out->eps_ms_total = h->prof_ms;
-    out->eps_latents = h->ctrl_host->nfe;
+    out->eps_latents = 0;
+    for (int n = 0; n < h->d.N; ++n) out->eps_latents += h->ctrl_host[n].nfe;
     return PA_OK;
 }
 

@@ -10,7 +10,10 @@ convention so every consumer sees the same arrays:
 * seed 0 -> initial latent ``x_init`` ~ N(0, 1), fp32;
 * seed 1 -> linear-network coefficients ``c_j`` ~ U(0.5, 1.5) per sampling step, fp32;
 * seed 2 -> patch-MLP weights, drawn in the order W1, Wt, W2, W3, each N(0, 1/fan_in)
-  in fp32, then stored as bf16 bit patterns (round to nearest even).
+  in fp32, then stored as bf16 bit patterns (round to nearest even);
+* seed 3 -> per-step noise z ~ N(0, 1) of the stochastic sampler, [N][T][D] fp32;
+* sample n of a batch draws its initial latent from seed 1000 + n (sample 0 of a batch
+  is therefore not the seed-0 latent of single-sample runs).
 
 The stand-in for the paper's Stable Diffusion v1.5 latents (4x64x64 for 512^2 images,
 Sec. 3.2) is plain N(0, 1) noise of the same shape; there is no text conditioning.
@@ -22,12 +25,25 @@ import numpy as np
 SEED_X_INIT = 0
 SEED_LINEAR_C = 1
 SEED_WEIGHTS = 2
+SEED_STEP_NOISE = 3
+SEED_BATCH_BASE = 1000
 
 
 def x_init(shape, seed: int = SEED_X_INIT) -> np.ndarray:
     """Initial latent of ``shape`` (C, H, W), fp32 N(0, 1)."""
     rng = np.random.default_rng(seed)
     return rng.standard_normal(tuple(shape)).astype(np.float32)
+
+
+def x_init_batch(shape, batch: int, base: int = SEED_BATCH_BASE) -> np.ndarray:
+    """Initial latents of a batch, [batch, C, H, W] fp32; sample n uses seed base + n."""
+    return np.stack([x_init(shape, base + n) for n in range(batch)])
+
+
+def step_noise(batch: int, T: int, D: int, seed: int = SEED_STEP_NOISE) -> np.ndarray:
+    """Per-step noise z[n][i] ~ N(0, 1) of the stochastic sampler, [batch, T, D] fp32."""
+    rng = np.random.default_rng(seed)
+    return rng.standard_normal((batch, T, D)).astype(np.float32)
 
 
 def linear_coefficients(T: int, seed: int = SEED_LINEAR_C) -> np.ndarray:

@@ -35,12 +35,13 @@ STATE_FRAC = 1e-4           # at most this fraction of state elements may differ
 FINAL_RTOL = 1e-4           # final latent, max-abs x RMS
 SUM_RTOL = 1e-11            # deviations/residuals: fp64 sums in different orders
 EPS_RTOL = 1e-2             # fresh network outputs, max-abs x RMS (bf16 rounding flips)
+REVISIT_THR = 0.05          # default threshold of the device's revisit counters
 
 
-def coefficients(T):
+def coefficients(T, eta=0.0):
     ab, t = sch.sampler_alpha_bar(T)
-    alpha, b = sch.ddim_coefficients(ab)
-    return ab, t, alpha, b
+    alpha, b, sigma = sch.step_coefficients(ab, eta)
+    return ab, t, alpha, b, sigma
 
 
 def oracle_network(wl, t_values):
@@ -101,26 +102,44 @@ def _check_slide(k, r_o, gpu, tau, log, state_err=0.0):
 
 
 class Run:
-    """A device run driven sweep by sweep with the step-locked check after each sweep."""
+    """A device run driven sweep by sweep with the step-locked check after each sweep.
+
+    ``batch`` > 1 drives one handle with that many samples (initial latents from
+    inputs.x_init_batch) and checks every sample that is still running after each batched
+    sweep. ``eta`` > 0 runs the stochastic step with the seeded step noise."""
 
     def __init__(self, wl, delta, *, verify_eps=8, seed_x=inputs.SEED_X_INIT, keep_eps=True,
-                 x_init=None):
+                 x_init=None, batch=1, eta=0.0):
         import torch
         self.wl, self.delta = wl, float(delta)
         self.T, self.P, self.D = wl.T, wl.window, wl.D
-        self.ab, self.t_values, self.alpha, self.b = coefficients(wl.T)
+        self.N, self.eta = int(batch), float(eta)
+        self.ab, self.t_values, self.alpha, self.b, self.sigma = coefficients(wl.T, self.eta)
         self.net = oracle_network(wl, self.t_values)
-        self.x_init = inputs.x_init(wl.latent, seed_x).reshape(-1) if x_init is None else x_init
+        if x_init is not None:
+            xs = np.asarray(x_init, np.float32).reshape(self.N, self.D)
+        elif self.N == 1:
+            xs = inputs.x_init(wl.latent, seed_x).reshape(1, -1)
+        else:
+            xs = inputs.x_init_batch(wl.latent, self.N).reshape(self.N, -1)
+        self.xs = xs
+        self.x_init = xs[0]
+        self.noise = None
+        if self.eta > 0.0:
+            self.Z = inputs.step_noise(self.N, self.T, self.D)
+            self.noise = [sp.step_noise_terms(self.sigma, self.Z[n]) for n in range(self.N)]
         self.log = Log()
-        self.records = []          # device trace records
-        self.eps_rows = []         # per sweep {t: device fresh output row} (patch-MLP)
+        self.records = [[] for _ in range(self.N)]    # device trace records per sample
+        self.eps_rows = [[] for _ in range(self.N)]   # per sample, per sweep {t: fresh output}
         self.verify_eps = verify_eps
         self.keep_eps = keep_eps
         self.eps_err = []          # max-abs/RMS of checked fresh outputs
         self.state_diffs = 0       # updated state elements that differ (by one ulp) at all
-        self.sampler = binding.from_workload(wl, delta, trace=True)
+        self.sampler = binding.from_workload(wl, delta, trace=True, batch=self.N, eta=self.eta)
         self.torch = torch
-        self.xd = torch.from_numpy(self.x_init.astype(np.float32)).cuda()
+        self.xd = torch.from_numpy(np.ascontiguousarray(xs, np.float32).reshape(-1)).cuda()
+        if self.eta > 0.0:
+            self.sampler.set_noise(torch.from_numpy(self.Z.reshape(-1)).cuda())
 
     def close(self):
         self.sampler.close()
@@ -128,89 +147,105 @@ class Run:
     def run(self):
         s = self.sampler
         s.reset(self.xd)
-        T, D = self.T, self.D
-        ost = sp.init_state(np.zeros(D, np.float32), T)     # rows are overwritten per sweep
-        newest = 0
+        T, D, N = self.T, self.D, self.N
+        ost = [sp.init_state(np.zeros(D, np.float32), T) for _ in range(N)]
+        newest = [0] * N
         k = 0
-        budget = self.verify_eps
+        self._budget = self.verify_eps
         while True:
-            st = s.stats()
-            if st["done"]:
+            active = [n for n in range(N) if not s.stats(n)["done"]]
+            if not active:
                 break
-            sw, e = st["window_start"], st["window_end"]
-            Xg, Xhg, Ehg, vg = s.read_state(sw, max(newest, sw) + 1)
-            ost.X[sw:sw + len(Xg)] = Xg
-            c1 = min(max(newest, sw) + 1, T)
-            ost.Xh[sw:c1] = Xhg
-            ost.Eh[sw:c1] = Ehg
-            ost.valid[:] = False
-            ost.valid[sw:c1] = vg
-            ost.s, ost.newest = sw, newest
+            pre = {}
+            for n in active:
+                st = s.stats(n)
+                sw, e = st["window_start"], st["window_end"]
+                Xg, Xhg, Ehg, vg = s.read_state(sw, max(newest[n], sw) + 1, n)
+                o = ost[n]
+                o.X[sw:sw + len(Xg)] = Xg
+                c1 = min(max(newest[n], sw) + 1, T)
+                o.Xh[sw:c1] = Xhg
+                o.Eh[sw:c1] = Ehg
+                o.valid[:] = False
+                o.valid[sw:c1] = vg
+                o.s, o.newest = sw, newest[n]
+                pre[n] = (sw, e)
             s.sweep(sync=True)
-            g = s.trace(k)
-            assert (g["s"], g["e"]) == (sw, e), f"sweep {k}: window mismatch"
-            # device post-state of the window
-            Xp, Xhp, Ehp, vp = s.read_state(sw, e + 1)
-            gpu_eps = {t: Ehp[t - sw].copy() for t in g["miss"]}
-            if self.wl.model == "linear":
-                eps_fn = self.net
-            else:
-                def eps_fn(Xb, steps, _g=gpu_eps):
-                    assert list(steps) == list(_g.keys()), "miss lists differ"
-                    return np.stack([_g[t] for t in steps]).astype(Xb.dtype)
-            # oracle: same sweep on the device's pre-state
-            sp.fill_new_states(ost.X, newest, e)
-            dev_o, hit_o = sp.cache_test(ost.X, ost.Xh, ost.valid, sw, e, self.delta)
-            hit = _check_hits(k, dev_o, g, self.delta, self.log)
-            X_before = ost.X[sw:e + 1].copy()
-            rec = sp.sweep(ost, self.P, self.delta, self.wl.tol, self.alpha, self.b, eps_fn,
-                           force_hit=hit)
-            assert rec["miss"] == g["miss"] and rec["m"] == g["m"], f"sweep {k}: miss list"
-            # updated states s+1..e: at most one fp32 ulp apart, rarely
-            ref = ost.X[sw + 1:e + 1]
-            diff = np.abs(Xp[1:].astype(np.float64) - ref.astype(np.float64))
-            ulp = np.spacing(np.abs(ref)).astype(np.float64)
-            assert np.all(diff <= STATE_ULPS * ulp), f"sweep {k}: states differ by {np.max(diff / ulp):.3g} ulp"
-            assert np.mean(diff > 0) <= STATE_FRAC, f"sweep {k}: {np.mean(diff > 0):.3g} of states differ"
-            self.state_diffs += int(np.count_nonzero(diff))
-            _check_slide(k, rec["r"], g, self.wl.tol, self.log, float(diff.max(initial=0.0)))
-            # cache: inputs of the misses are the pre-update states, hits untouched
-            for j in range(e - sw):
-                t = sw + j
-                if t in gpu_eps:
-                    assert np.array_equal(Xhp[j], X_before[j]), f"sweep {k}: cached input of miss {t}"
-                    assert vp[j]
-                else:
-                    assert np.array_equal(Xhp[j], ost.Xh[t]) and np.array_equal(Ehp[j], ost.Eh[t])
-            if self.wl.model == "linear":
-                for t, row in gpu_eps.items():     # exact fp32 product on both sides
-                    assert np.array_equal(row, ost.Eh[t]), f"sweep {k}: linear output of {t}"
-            elif budget > 0 and g["m"] > 0:
-                picks = sorted({g["miss"][0], g["miss"][-1]})
-                for t in picks[:budget]:
-                    ref = self.net.eval_one(X_before[t - sw], t)
-                    sc = max(rms(ref), 1e-30)
-                    e_rel = float(np.max(np.abs(gpu_eps[t].astype(np.float64) - ref)) / sc)
-                    self.eps_err.append(e_rel)
-                    assert e_rel <= EPS_RTOL, f"sweep {k}: network output of {t} off by {e_rel:.3g} x RMS"
-                    budget -= 1
-            self.records.append(g)
-            if self.keep_eps and self.wl.model != "linear":
-                self.eps_rows.append(gpu_eps)
-            newest = max(newest, e)
+            for n in active:
+                sw, e = pre[n]
+                self._check_sweep(n, k, sw, e, ost[n], newest[n])
+                newest[n] = max(newest[n], e)
             k += 1
             assert k <= T, "more sweeps than steps"
         self.stats = s.stats()
-        Xfin, _, _, _ = s.read_state(T, T + 1)
-        self.x_T = Xfin[0].copy()
+        self.stats_n = [s.stats(n) for n in range(N)]
+        self.x_T_all = [s.read_state(T, T + 1, n)[0][0].copy() for n in range(N)]
+        self.x_T = self.x_T_all[0]
         return self
 
-    def follow(self):
-        """Oracle trajectory of its own (eps-locked for the patch-MLP); returns x_T error / RMS."""
+    def _check_sweep(self, n, k, sw, e, ost, newest):
+        s = self.sampler
+        g = s.trace(k, n)
+        assert (g["s"], g["e"]) == (sw, e), f"sample {n} sweep {k}: window mismatch"
+        # device post-state of the window
+        Xp, Xhp, Ehp, vp = s.read_state(sw, e + 1, n)
+        gpu_eps = {t: Ehp[t - sw].copy() for t in g["miss"]}
+        if self.wl.model == "linear":
+            eps_fn = self.net
+        else:
+            def eps_fn(Xb, steps, _g=gpu_eps):
+                assert list(steps) == list(_g.keys()), "miss lists differ"
+                return np.stack([_g[t] for t in steps]).astype(Xb.dtype)
+        noise = None if self.noise is None else self.noise[n]
+        # oracle: same sweep on the device's pre-state
+        sp.fill_new_states(ost.X, newest, e)
+        dev_o, hit_o = sp.cache_test(ost.X, ost.Xh, ost.valid, sw, e, self.delta)
+        hit = _check_hits(k, dev_o, g, self.delta, self.log)
+        X_before = ost.X[sw:e + 1].copy()
+        rec = sp.sweep(ost, self.P, self.delta, self.wl.tol, self.alpha, self.b, eps_fn,
+                       force_hit=hit, noise=noise)
+        assert rec["miss"] == g["miss"] and rec["m"] == g["m"], f"sample {n} sweep {k}: miss list"
+        # updated states s+1..e: at most one fp32 ulp apart, rarely
+        ref = ost.X[sw + 1:e + 1]
+        diff = np.abs(Xp[1:].astype(np.float64) - ref.astype(np.float64))
+        ulp = np.spacing(np.abs(ref)).astype(np.float64)
+        assert np.all(diff <= STATE_ULPS * ulp), f"sample {n} sweep {k}: states differ by {np.max(diff / ulp):.3g} ulp"
+        assert np.mean(diff > 0) <= STATE_FRAC, f"sample {n} sweep {k}: {np.mean(diff > 0):.3g} of states differ"
+        self.state_diffs += int(np.count_nonzero(diff))
+        _check_slide(k, rec["r"], g, self.wl.tol, self.log, float(diff.max(initial=0.0)))
+        # cache: inputs of the misses are the pre-update states, hits untouched
+        for j in range(e - sw):
+            t = sw + j
+            if t in gpu_eps:
+                assert np.array_equal(Xhp[j], X_before[j]), f"sample {n} sweep {k}: cached input of miss {t}"
+                assert vp[j]
+            else:
+                assert np.array_equal(Xhp[j], ost.Xh[t]) and np.array_equal(Ehp[j], ost.Eh[t])
+        if self.wl.model == "linear":
+            for t, row in gpu_eps.items():     # exact fp32 product on both sides
+                assert np.array_equal(row, ost.Eh[t]), f"sample {n} sweep {k}: linear output of {t}"
+        elif self._budget > 0 and g["m"] > 0:
+            picks = sorted({g["miss"][0], g["miss"][-1]})
+            for t in picks[:self._budget]:
+                ref = self.net.eval_one(X_before[t - sw], t)
+                sc = max(rms(ref), 1e-30)
+                e_rel = float(np.max(np.abs(gpu_eps[t].astype(np.float64) - ref)) / sc)
+                self.eps_err.append(e_rel)
+                assert e_rel <= EPS_RTOL, f"sample {n} sweep {k}: network output of {t} off by {e_rel:.3g} x RMS"
+                self._budget -= 1
+        self.records[n].append(g)
+        if self.keep_eps and self.wl.model != "linear":
+            self.eps_rows[n].append(gpu_eps)
+
+    def follow(self, n=0):
+        """Oracle trajectory of its own for sample n (eps-locked for the patch-MLP); returns
+        the x_T error / RMS. Also checks the device's revisit counters against the oracle's."""
         T, P = self.T, self.P
-        st = sp.init_state(self.x_init, T)
+        st = sp.init_state(self.xs[n], T)
+        noise = None if self.noise is None else self.noise[n]
         log = Log()
-        for k, g in enumerate(self.records):
+        trace = []
+        for k, g in enumerate(self.records[n]):
             assert st.s == g["s"], f"follow sweep {k}: window start {st.s} vs {g['s']}"
             e = sp.window_end(st.s, T, P)
             sp.fill_new_states(st.X, st.newest, e)
@@ -219,11 +254,13 @@ class Run:
             if self.wl.model == "linear":
                 eps_fn = self.net
             else:
-                rows = self.eps_rows[k]
+                rows = self.eps_rows[n][k]
                 def eps_fn(Xb, steps, _r=rows):
                     assert list(steps) == list(_r.keys())
                     return np.stack([_r[t] for t in steps]).astype(Xb.dtype)
-            rec = sp.sweep(st, P, self.delta, self.wl.tol, self.alpha, self.b, eps_fn, force_hit=hit)
+            rec = sp.sweep(st, P, self.delta, self.wl.tol, self.alpha, self.b, eps_fn,
+                           force_hit=hit, noise=noise)
+            trace.append(rec)
             assert rec["miss"] == g["miss"]
             c_o = rec["c"]
             if c_o != g["c"]:
@@ -231,8 +268,17 @@ class Run:
                 assert _in_band(rec["r"][j], self.wl.tol), f"follow sweep {k}: slide differs"
                 log.flip("tau", k, j, rec["r"][j], self.wl.tol)
                 st.s = g["s_next"]
-        assert st.done and st.nfe == self.stats["nfe"] and st.hits == self.stats["hits"]
+        stn = self.stats_n[n]
+        assert st.done and st.nfe == stn["nfe"] and st.hits == stn["hits"]
+        # revisit counters (default threshold 0.05): the oracle's count from its own trace;
+        # a deviation within the band of the threshold may fall either way.
+        req, rev, below = sp.revisit_counts(trace, REVISIT_THR)
+        assert req == stn["nfe"] + stn["hits"] and rev == stn["revisits"]
+        near = sum(int(np.count_nonzero(np.abs(np.nan_to_num(np.asarray(r["dev"]), nan=-1.0) - REVISIT_THR)
+                                        <= BAND * REVISIT_THR)) for r in trace)
+        assert abs(below - stn["revisits_below"]) <= near, (below, stn["revisits_below"])
         ref = st.X[T].astype(np.float64)
-        err = float(np.max(np.abs(self.x_T.astype(np.float64) - ref)) / max(rms(ref), 1e-30))
+        x_T = self.x_T_all[n]
+        err = float(np.max(np.abs(x_T.astype(np.float64) - ref)) / max(rms(ref), 1e-30))
         self.follow_log = log
         return err

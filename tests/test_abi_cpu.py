@@ -22,7 +22,7 @@ def _declared():
 def test_library_exports_every_declared_symbol():
     lib = B.load_library()
     names = _declared()
-    assert len(names) == 12
+    assert len(names) == 17
     assert sorted(B.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -36,10 +36,10 @@ def test_status_strings():
 
 
 def _create(shape=(1, 4, 8, 8), T=10, window=4, delta=0.05, tol=1e-3, kind=B.PA_EPS_LINEAR,
-            hidden=1024, patch=2, temb_dim=128, sched=None, flags=0, null_c=False):
+            hidden=1024, patch=2, temb_dim=128, sched=None, flags=0, null_c=False, eta=0.0):
     lib = B.load_library()
     sh = (C.c_int32 * 4)(*shape)
-    sc = sched or B.Schedule(B.PA_SCHED_SCALED_LINEAR, 0.00085, 0.012, 1000, 0, 1, None, None)
+    sc = sched or B.Schedule(B.PA_SCHED_SCALED_LINEAR, 0.00085, 0.012, 1000, 0, 1, None, None, eta)
     c = np.ones(max(T, 1), np.float32)
     w = {k: np.zeros(1, np.uint16) for k in ("w1", "wt", "w2", "w3")}
     em = B.EpsModel(kind, None if null_c else c.ctypes.data_as(C.POINTER(C.c_float)), patch,
@@ -52,7 +52,11 @@ def _create(shape=(1, 4, 8, 8), T=10, window=4, delta=0.05, tol=1e-3, kind=B.PA_
 
 
 @pytest.mark.parametrize("kw,frag", [
-    (dict(shape=(2, 4, 8, 8)), "batch"),
+    (dict(shape=(0, 4, 8, 8)), "batch"),
+    (dict(shape=(B.PA_MAX_BATCH + 1, 4, 8, 8)), "batch"),
+    (dict(eta=-0.5), "eta"),
+    (dict(eta=1.5), "eta"),
+    (dict(eta=float("nan")), "eta"),
     (dict(shape=(1, 3, 3, 3)), "multiple of 4"),
     (dict(T=0, window=1), "T must"),
     (dict(window=0), "window"),
@@ -93,7 +97,7 @@ def test_explicit_schedule_validation():
     ab = np.array([0.5, 0.7, 1.5], np.float64)       # > 1: invalid
     tv = np.array([10, 5], np.int32)
     sc = B.Schedule(B.PA_SCHED_EXPLICIT, 0, 0, 0, 0, 0, ab.ctypes.data_as(C.POINTER(C.c_double)),
-                    tv.ctypes.data_as(C.POINTER(C.c_int32)))
+                    tv.ctypes.data_as(C.POINTER(C.c_int32)), 0.0)
     rc, h, msg = _create(T=2, window=2, sched=sc)
     assert rc == B.PA_ERR_INVALID_ARG and "alpha_bar[2]" in msg
 
@@ -105,4 +109,41 @@ def test_null_handle_calls_fail_cleanly():
     assert lib.paraanya_sample(None, None, None) == B.PA_ERR_INVALID_ARG
     st = B.Stats()
     assert lib.paraanya_stats(None, C.byref(st)) == B.PA_ERR_INVALID_ARG
+    assert lib.paraanya_stats_sample(None, 0, C.byref(st)) == B.PA_ERR_INVALID_ARG
+    assert lib.paraanya_set_noise(None, None) == B.PA_ERR_INVALID_ARG
+    assert lib.paraanya_set_revisit_threshold(None, 0.05) == B.PA_ERR_INVALID_ARG
+    tr = B.SweepTrace()
+    assert lib.paraanya_trace_sample(None, 0, 0, C.byref(tr)) == B.PA_ERR_INVALID_ARG
+    assert lib.paraanya_read_state_sample(None, 0, 0, 1, None, None, None, None) == B.PA_ERR_INVALID_ARG
     lib.paraanya_destroy(None)   # NULL-safe
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The binding's ctypes structures have the sizes and field offsets of the header's C
+    structs (compiled here with the host C compiler)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    fields = {"pa_schedule_t": (B.Schedule, ["kind", "beta_start", "train_steps", "alpha_bar", "t_values", "eta"]),
+              "pa_stats_t": (B.Stats, ["nfe", "sweeps", "window_start", "nonfinite", "revisits", "revisits_below"]),
+              "pa_sweep_trace_t": (B.SweepTrace, ["s", "sweep", "dev", "resid", "miss_idx", "hit"]),
+              "pa_eps_model_t": (B.EpsModel, ["kind", "c", "hidden", "w1", "w3"]),
+              "pa_ktimes_t": (B.KTimes, ["launches", "eps_ms_total", "eps_latents"])}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "paraanya.h"', "int main(void) {"]
+    for st, (_, fs) in fields.items():
+        lines.append(f'printf("%zu\\n", sizeof({st}));')
+        lines += [f'printf("%zu\\n", offsetof({st}, {f}));' for f in fs]
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    vals = [int(v) for v in subprocess.run([str(exe)], check=True, capture_output=True,
+                                           text=True).stdout.split()]
+    it = iter(vals)
+    for st, (cls, fs) in fields.items():
+        assert next(it) == C.sizeof(cls), st
+        for f in fs:
+            assert next(it) == getattr(cls, f).offset, f"{st}.{f}"

@@ -87,8 +87,8 @@ def test_explicit_schedule_matches_scaled_linear(gpu_lib):
     ab, t = sch.sampler_alpha_bar(wl.T)
     x = _x(wl)
     with B.from_workload(wl) as s1, B.from_workload(wl, schedule={"alpha_bar": ab, "t_values": t}) as s2:
-        a1, b1, _ = s1.coefficients()
-        a2, b2, _ = s2.coefficients()
+        a1, b1, _, _ = s1.coefficients()
+        a2, b2, _, _ = s2.coefficients()
         assert np.array_equal(a1, a2) and np.array_equal(b1, b2)
         assert np.array_equal(s1.sample(x).cpu().numpy(), s2.sample(x).cpu().numpy())
 
@@ -99,7 +99,7 @@ def test_uploaded_coefficients_are_rounded_oracle_values(T, gpu_lib):
     ab, t = sch.sampler_alpha_bar(T)
     alpha, b = sch.ddim_coefficients(ab)
     with B.from_workload(wl) as s:
-        a32, b32, _ = s.coefficients()
+        a32, b32, _, _ = s.coefficients()
     # Same fp64 definition on both sides: bit-identical coefficient tables.
     assert np.array_equal(a32, alpha) and np.array_equal(b32, b)
 
@@ -109,7 +109,7 @@ def test_time_embedding_table(gpu_lib):
     ab, t = sch.sampler_alpha_bar(wl.T)
     net = em.PatchMLP(inputs.mlp_weights(wl.hidden), t, wl.latent)
     with B.from_workload(wl) as s:
-        _, _, temb = s.coefficients()
+        _, _, _, temb = s.coefficients()
     diff = np.abs(temb.astype(np.float64) - net.temb.astype(np.float64))
     assert np.all(diff <= np.abs(net.temb) * 2.0 ** -23 + 1e-30)
 
@@ -123,3 +123,105 @@ def test_profile_counts_launches(gpu_lib):
     # sample() may enqueue a sweep or two past done; those network launches exit at once.
     assert kt["launches"] >= st["sweeps"] and kt["eps_latents"] == st["nfe"]
     assert kt["eps_ms_total"] > 0
+
+
+@pytest.mark.parametrize("T,eta", [(10, 1.0), (100, 1.0), (1000, 1.0), (50, 0.5)])
+def test_stochastic_coefficients_are_oracle_values(T, eta, gpu_lib):
+    wl = W.TINY_LINEAR.with_(T=T, window=min(4, T))
+    ab, t = sch.sampler_alpha_bar(T)
+    alpha, b, sigma = sch.step_coefficients(ab, eta)
+    with B.from_workload(wl, eta=eta) as s:
+        a, bb, sg, _ = s.coefficients()
+    assert np.array_equal(a, alpha) and np.array_equal(bb, b) and np.array_equal(sg, sigma)
+
+
+def test_stochastic_handle_needs_noise(gpu_lib):
+    wl = W.TINY_LINEAR
+    x = _x(wl)
+    with B.from_workload(wl, eta=1.0) as s:
+        with pytest.raises(B.PAError) as ei:
+            s.sample(x)
+        assert ei.value.code == B.PA_ERR_STATE
+        z = torch.from_numpy(inputs.step_noise(1, wl.T, wl.D).reshape(-1)).cuda()
+        s.set_noise(z)
+        out1 = s.sample(x).cpu().numpy()
+        z2 = torch.zeros_like(z)
+        s.set_noise(z2)
+        out0 = s.sample(x).cpu().numpy()
+    assert not np.array_equal(out1, out0)          # the noise term is live
+    with B.from_workload(wl) as s:
+        with pytest.raises(B.PAError) as ei:
+            s.set_noise(torch.zeros(wl.T * wl.D, device="cuda"))
+        assert ei.value.code == B.PA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("wl,eta", [(W.TINY_LINEAR, 0.0), (W.SMALL_MLP, 0.0), (W.SD_MLP, 0.0),
+                                    (W.TINY_LINEAR, 1.0), (W.SMALL_MLP, 1.0)],
+                         ids=["linear", "mlp_small", "mlp_sd", "linear_ddpm", "mlp_small_ddpm"])
+def test_batch_equals_independent_samples(wl, eta, gpu_lib):
+    """A handle with N samples gives each sample exactly what a single-sample handle gives
+    it: the same final latent bit for bit, counters and sweep traces."""
+    N = 4
+    xb = inputs.x_init_batch(wl.latent, N).reshape(N, -1)
+    Z = inputs.step_noise(N, wl.T, wl.D) if eta > 0 else None
+    with B.from_workload(wl, batch=N, eta=eta, trace=True) as s:
+        if Z is not None:
+            s.set_noise(torch.from_numpy(Z.reshape(-1)).cuda())
+        outb = s.sample(torch.from_numpy(xb.reshape(-1)).cuda()).cpu().numpy().reshape(N, -1)
+        stb = [s.stats(n) for n in range(N)]
+        trb = [s.traces(n) for n in range(N)]
+        agg = s.stats()
+    for n in range(N):
+        with B.from_workload(wl, eta=eta, trace=True) as s1:
+            if Z is not None:
+                s1.set_noise(torch.from_numpy(Z[n].reshape(-1)).cuda())
+            out1 = s1.sample(torch.from_numpy(xb[n]).cuda()).cpu().numpy()
+            st1 = s1.stats()
+            tr1 = s1.traces()
+        assert np.array_equal(outb[n], out1), f"sample {n}"
+        assert stb[n] == st1, (n, stb[n], st1)
+        assert len(trb[n]) == len(tr1)
+        for a, b in zip(trb[n], tr1):
+            assert a["miss"] == b["miss"] and a["c"] == b["c"]
+            assert np.array_equal(a["dev"], b["dev"], equal_nan=True) and np.array_equal(a["r"], b["r"])
+    assert agg["nfe"] == sum(x["nfe"] for x in stb) and agg["done"]
+    assert agg["sweeps"] == max(x["sweeps"] for x in stb)
+    assert agg["window_start"] == min(x["window_start"] for x in stb)
+
+
+def test_revisit_threshold(gpu_lib):
+    wl = W.SMALL_MLP
+    x = _x(wl)
+    with B.from_workload(wl, 0.0) as s:
+        s.sample(x)
+        st = s.stats()
+        assert st["revisits"] == st["nfe"] + st["hits"] - wl.T
+        s.set_revisit_threshold(math.inf)
+        s.sample(x)
+        assert s.stats()["revisits_below"] == s.stats()["revisits"]
+        s.set_revisit_threshold(0.0)
+        s.sample(x)
+        assert s.stats()["revisits_below"] == 0
+        with pytest.raises(B.PAError) as ei:
+            s.set_revisit_threshold(-1.0)
+        assert ei.value.code == B.PA_ERR_INVALID_ARG
+        with pytest.raises(B.PAError) as ei:
+            s.set_revisit_threshold(float("nan"))
+        assert ei.value.code == B.PA_ERR_INVALID_ARG
+
+
+def test_batch_argument_checks(gpu_lib):
+    wl = W.TINY_LINEAR
+    with B.from_workload(wl, batch=3, trace=True) as s:
+        xb = torch.from_numpy(inputs.x_init_batch(wl.latent, 3).reshape(-1)).cuda()
+        s.sample(xb)
+        for bad in (-1, 3):
+            with pytest.raises(B.PAError) as ei:
+                s.stats(bad)
+            assert ei.value.code == B.PA_ERR_INVALID_ARG
+            with pytest.raises(B.PAError) as ei:
+                s.trace(0, bad)
+            assert ei.value.code == B.PA_ERR_INVALID_ARG
+            with pytest.raises(B.PAError) as ei:
+                s.read_state(0, 1, bad)
+            assert ei.value.code == B.PA_ERR_INVALID_ARG

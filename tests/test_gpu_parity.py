@@ -45,31 +45,50 @@ CASES = [
     ("mlp_small_delta0", W.SMALL_MLP, 0.0),
     ("mlp_sd", W.SD_MLP, 0.05),
     ("mlp_sd_delta0", W.SD_MLP, 0.0),
+    # several samples per handle: every sample step-locked and followed on its own
+    ("batch5_tiny", LIN, 0.05, dict(batch=5)),
+    ("batch3_ragged", Workload("lin_3x5x4", (3, 5, 4), 12, 5, 0.1, 1e-3, "linear"), 0.1, dict(batch=3)),
+    ("batch3_mlp_small", W.SMALL_MLP, 0.05, dict(batch=3)),
+    ("batch4_mlp_sd", W.SD_MLP, 0.05, dict(batch=4)),
+    # stochastic step (ancestral DDPM) with pre-drawn step noise
+    ("ddpm_tiny", LIN, 0.05, dict(eta=1.0)),
+    ("ddpm_tiny_delta0", LIN, 0.0, dict(eta=1.0)),
+    ("ddpm_window1", LIN.with_(window=1), 0.05, dict(eta=1.0)),
+    ("ddpm_batch3_tiny", LIN, 0.05, dict(eta=1.0, batch=3)),
+    ("ddpm_mlp_small", W.SMALL_MLP, 0.05, dict(eta=1.0)),
+    ("ddpm_eta_half", W.SMALL_MLP, 0.05, dict(eta=0.5)),
 ]
+CASES = [c if len(c) == 4 else (*c, {}) for c in CASES]
 
 
-@pytest.mark.parametrize("name,wl,delta", CASES, ids=[c[0] for c in CASES])
-def test_parity(name, wl, delta, gpu_lib):
-    print(f"[parity] {name}: {wl.name} delta={delta}", flush=True)
-    run = H.Run(wl, delta, verify_eps=6).run()
+@pytest.mark.parametrize("name,wl,delta,kw", CASES, ids=[c[0] for c in CASES])
+def test_parity(name, wl, delta, kw, gpu_lib):
+    print(f"[parity] {name}: {wl.name} delta={delta} {kw}", flush=True)
+    run = H.Run(wl, delta, verify_eps=6, **kw).run()
     try:
-        st = run.stats
-        assert st["done"] and st["sweeps"] == len(run.records) <= wl.T
-        assert st["nfe"] >= wl.T and st["nfe"] == sum(r["m"] for r in run.records)
-        assert st["hits"] == sum(r["e"] - r["s"] - r["m"] for r in run.records)
-        if delta == 0.0:
-            assert st["hits"] == 0
-        if delta == INF:
-            assert st["nfe"] == wl.T
-        if wl.window == 1:
-            assert st["sweeps"] == wl.T and st["nfe"] == wl.T
-        assert run.records[0]["m"] == min(wl.window, wl.T)
-        err = run.follow()
-        assert err <= H.FINAL_RTOL, f"final latent off by {err:.3g} x RMS"
-        print(f"[parity] {name}: sweeps={st['sweeps']} nfe={st['nfe']} hits={st['hits']} "
-              f"final_err={err:.2e} eps_err_max={max(run.eps_err, default=0):.2e} "
-              f"state_ulp_diffs={run.state_diffs} "
-              f"flips={len(run.log.flips) + len(run.follow_log.flips)}", flush=True)
+        for n in range(run.N):
+            st = run.stats_n[n]
+            recs = run.records[n]
+            assert st["done"] and st["sweeps"] == len(recs) <= wl.T
+            assert st["nfe"] >= wl.T and st["nfe"] == sum(r["m"] for r in recs)
+            assert st["hits"] == sum(r["e"] - r["s"] - r["m"] for r in recs)
+            if delta == 0.0:
+                assert st["hits"] == 0
+            if delta == INF:
+                assert st["nfe"] == wl.T
+            if wl.window == 1:
+                assert st["sweeps"] == wl.T and st["nfe"] == wl.T
+            assert recs[0]["m"] == min(wl.window, wl.T)
+            err = run.follow(n)
+            assert err <= H.FINAL_RTOL, f"sample {n}: final latent off by {err:.3g} x RMS"
+            print(f"[parity] {name}[{n}]: sweeps={st['sweeps']} nfe={st['nfe']} hits={st['hits']} "
+                  f"revisits={st['revisits']} below={st['revisits_below']} "
+                  f"final_err={err:.2e} eps_err_max={max(run.eps_err, default=0):.2e} "
+                  f"state_ulp_diffs={run.state_diffs} "
+                  f"flips={len(run.log.flips) + len(run.follow_log.flips)}", flush=True)
+        agg = run.stats
+        assert agg["nfe"] == sum(x["nfe"] for x in run.stats_n)
+        assert agg["sweeps"] == max(x["sweeps"] for x in run.stats_n)
     finally:
         run.close()
 
@@ -85,6 +104,21 @@ def test_long_window_sd(gpu_lib):
         assert err <= H.FINAL_RTOL
         assert run.stats["nfe"] >= wl.T
         print(f"[parity] long: sweeps={run.stats['sweeps']} nfe={run.stats['nfe']} "
+              f"hits={run.stats['hits']} final_err={err:.2e}", flush=True)
+    finally:
+        run.close()
+
+
+def test_long_ddpm_window64(gpu_lib):
+    """The window study's stochastic setting at full size: ancestral DDPM over T=1000 with a
+    window of 64 on the SD latent shape, step-locked and followed to the final latent."""
+    wl = W.LONG_MLP.with_(window=64)
+    print(f"[parity] long ddpm: {wl.name} P=64 eta=1", flush=True)
+    run = H.Run(wl, 0.05, verify_eps=6, eta=1.0).run()
+    try:
+        err = run.follow()
+        assert err <= H.FINAL_RTOL
+        print(f"[parity] long ddpm: sweeps={run.stats['sweeps']} nfe={run.stats['nfe']} "
               f"hits={run.stats['hits']} final_err={err:.2e}", flush=True)
     finally:
         run.close()
