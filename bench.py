@@ -34,6 +34,7 @@ if ROOT not in sys.path:
 
 METRIC = "cached Picard sweeps/s + ε evals/s at 4×64×64, T=100; NFE saved vs δ=0"
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0              # MI355X HBM3E
 PRIMARY_DELTA = 0.05
 
 
@@ -86,8 +87,8 @@ def timed_samples(sampler, x, steps, warmup, torch):
         sampler.sample(x, out)
     torch.cuda.synchronize()
     sweeps = nfe = hits = revisits = below = 0
-    eps_ms = 0.0
-    launches = 0
+    eps_ms = picard_ms = slide_ms = 0.0
+    launches = solver_launches = 0
     t0 = time.perf_counter()
     for _ in range(steps):
         sampler.sample(x, out)
@@ -100,14 +101,38 @@ def timed_samples(sampler, x, steps, warmup, torch):
         below += st["revisits_below"]
         eps_ms += kt["eps_ms_total"]
         launches += kt["launches"]
+        picard_ms += kt["picard_ms_total"]
+        slide_ms += kt["slide_ms_total"]
+        solver_launches += kt["solver_launches"]
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     return {"seconds": dt, "sweeps": sweeps, "nfe": nfe, "hits": hits, "eps_ms": eps_ms,
-            "launches": launches, "revisits": revisits, "revisits_below": below, "out": out}
+            "launches": launches, "revisits": revisits, "revisits_below": below,
+            "picard_ms": picard_ms, "slide_ms": slide_ms, "solver_launches": solver_launches,
+            "out": out}
 
 
-def run_case(wl, delta, steps, warmup, torch, weights, *, batch=1, eta=0.0):
-    """Timed samples of one configuration (profiled handle: kernel-attached events)."""
+def solver_kernels(r, D):
+    """HBM view of the two solver kernels from their event times (a separate run whose
+    handle times them: their events add stream time, so it is not the headline run).
+
+    k_picard's algorithmic bytes per sweep are the Picard update's (3W + 1) * 4D (read the
+    W + 1 window states and the W assembled outputs, write W states) plus 8D per miss (the
+    Eq. (7) cache writes of input and output); the cache-test re-reads it avoids are not
+    counted. Summed over a run: 4D * (3 * (nfe + hits) + sweeps + 2 * nfe). k_slide moves
+    only the fp64 partial sums and the control block: it is bound by latency, not bytes."""
+    byts = 4.0 * D * (3 * (r["nfe"] + r["hits"]) + r["sweeps"] + 2 * r["nfe"])
+    n = max(r["solver_launches"], 1)
+    gbs = byts / (r["picard_ms"] * 1e-3) / 1e9 if r["picard_ms"] > 0 else None
+    return {"k_picard": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": (gbs / PEAK_HBM_GBS) if gbs else None,
+                         "bytes_per_launch": byts / n, "avg_launch_us": 1e3 * r["picard_ms"] / n},
+            "k_slide": {"bound": "latency", "avg_launch_us": 1e3 * r["slide_ms"] / n}}
+
+
+def run_case(wl, delta, steps, warmup, torch, weights, *, batch=1, eta=0.0, solver=False):
+    """Timed samples of one configuration (profiled handle: kernel-attached events on the
+    network launches; with ``solver`` on the Picard and slide launches too)."""
     from paper_2609_36522_amd import binding, inputs
     if batch == 1:
         xs = inputs.x_init(wl.latent).reshape(-1)
@@ -115,7 +140,7 @@ def run_case(wl, delta, steps, warmup, torch, weights, *, batch=1, eta=0.0):
         xs = inputs.x_init_batch(wl.latent, batch).reshape(-1)
     x = torch.from_numpy(xs).cuda()
     with binding.from_workload(wl, delta, seed_weights=weights, profile=True, batch=batch,
-                               eta=eta) as s:
+                               eta=eta, profile_solver=solver) as s:
         if eta > 0:
             s.set_noise(torch.from_numpy(inputs.step_noise(batch, wl.T, wl.D).reshape(-1)).cuda())
         return timed_samples(s, x, steps, warmup, torch)
@@ -195,7 +220,9 @@ def main():
             "eps_evals_per_s": rb["nfe"] / rb["seconds"],
             "batched_sweeps_per_batch": rb["sweeps"] / bsteps,
             "nfe_per_sample": rb["nfe"] / (nb * bsteps),
-            "eps_kernel_tflops": (rb["nfe"] * fpe) / (rb["eps_ms"] * 1e-3) / 1e12 if rb["eps_ms"] > 0 else None}
+            "eps_kernel_tflops": (rb["nfe"] * fpe) / (rb["eps_ms"] * 1e-3) / 1e12 if rb["eps_ms"] > 0 else None,
+            "solver_kernels": solver_kernels(
+                run_case(wl, PRIMARY_DELTA, 3, 1, torch, weights, batch=nb, solver=True), wl.D)}
         print(f"[bench] batch {nb}: {extras['batched']['ms_per_batch']:.3f} ms/batch, "
               f"{extras['batched']['samples_per_s']:.0f} samples/s", file=sys.stderr, flush=True)
         # the window study's stochastic setting
@@ -263,6 +290,8 @@ def main():
                                "eps_kernel_tflops": ((r["nfe"] * fpe) / (r["eps_ms"] * 1e-3) / 1e12
                                                      if r["eps_ms"] > 0 else None)}
                       for d, r in per_delta.items()},
+        "solver_kernels": solver_kernels(
+            run_case(wl, PRIMARY_DELTA, 10, 1, torch, weights, solver=True), wl.D),
         "roofline": {"bound": "mfma", "kernel": "k_eps_mlp<1024>",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),

@@ -113,6 +113,8 @@ typedef struct {
 /* ------------------------------------------------------------------ create flags */
 #define PA_FLAG_TRACE   1u   /* keep a per-sweep trace record (paraanya_trace) */
 #define PA_FLAG_PROFILE 2u   /* time every network launch with HIP events (paraanya_kernel_times) */
+#define PA_FLAG_PROFILE_SOLVER 4u  /* with PA_FLAG_PROFILE: time the Picard and slide launches
+                                      too (their events add ~7 us per sweep of stream time) */
 
 typedef struct paraanya paraanya_t;
 
@@ -149,11 +151,15 @@ typedef struct {
     uint8_t hit[PA_MAX_WINDOW];       /* Eq. (5) hit mask per slot */
 } pa_sweep_trace_t;
 
-/* Device time of the network launches since reset (PA_FLAG_PROFILE). */
+/* Device time of the kernels since reset (PA_FLAG_PROFILE): each launch carries start/stop
+ * events on the handle's stream. */
 typedef struct {
-    int64_t launches;
-    double  eps_ms_total;   /* summed kernel durations of the network launches */
-    int64_t eps_latents;    /* latents evaluated by those launches (= nfe) */
+    int64_t launches;         /* network launches */
+    double  eps_ms_total;     /* summed kernel durations of the network launches */
+    int64_t eps_latents;      /* latents evaluated by those launches (= nfe) */
+    int64_t solver_launches;  /* Picard launches (= window-slide launches) */
+    double  picard_ms_total;  /* summed durations of the drift / Picard / cache-update kernel */
+    double  slide_ms_total;   /* summed durations of the residual / slide / hit-test kernel */
 } pa_ktimes_t;
 
 /* ------------------------------------------------------------------ entry points */
@@ -230,7 +236,7 @@ PA_API int paraanya_read_state_sample(paraanya_t* h, int32_t n, int32_t t0, int3
  * fp32 time-embedding table e[T][hidden]. */
 PA_API int paraanya_coefficients(paraanya_t* h, double* alpha, double* b, double* sigma, float* temb);
 
-/* Network-launch timings since reset (PA_FLAG_PROFILE); synchronizes. STATE without it. */
+/* Kernel timings since reset (PA_FLAG_PROFILE); synchronizes. STATE without it. */
 PA_API int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out);
 
 /* Free every resource of the handle (synchronizes its stream first). NULL-safe. */

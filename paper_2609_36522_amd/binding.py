@@ -31,6 +31,7 @@ PA_EPS_LINEAR = 0
 PA_EPS_PATCH_MLP = 1
 PA_FLAG_TRACE = 1
 PA_FLAG_PROFILE = 2
+PA_FLAG_PROFILE_SOLVER = 4
 
 EXPORTED = ("paraanya_create", "paraanya_reset", "paraanya_sweep", "paraanya_sample",
             "paraanya_stats", "paraanya_trace", "paraanya_read_state", "paraanya_coefficients",
@@ -81,7 +82,8 @@ class SweepTrace(C.Structure):
 
 class KTimes(C.Structure):
     _fields_ = [("launches", C.c_int64), ("eps_ms_total", C.c_double),
-                ("eps_latents", C.c_int64)]
+                ("eps_latents", C.c_int64), ("solver_launches", C.c_int64),
+                ("picard_ms_total", C.c_double), ("slide_ms_total", C.c_double)]
 
 
 _LIB = None
@@ -153,7 +155,7 @@ class Sampler:
 
     def __init__(self, latent, T, window, delta, tol, model, *, c=None, weights=None,
                  hidden=0, schedule=None, stream=None, trace=False, profile=False, batch=1,
-                 eta=0.0):
+                 eta=0.0, profile_solver=False):
         import torch
         self.lib = load_library()
         self.latent = tuple(int(v) for v in latent)
@@ -185,7 +187,8 @@ class Sampler:
                           _ptr(ws["w2"], C.c_uint16), _ptr(ws["w3"], C.c_uint16))
         else:
             raise ValueError(f"unknown model {model!r}")
-        flags = (PA_FLAG_TRACE if trace else 0) | (PA_FLAG_PROFILE if profile else 0)
+        flags = (PA_FLAG_TRACE if trace else 0) | (PA_FLAG_PROFILE if profile else 0) | \
+            (PA_FLAG_PROFILE | PA_FLAG_PROFILE_SOLVER if profile_solver else 0)
         h = C.c_void_p()
         _check(self.lib.paraanya_create(shape, self.T, C.byref(sc), self.P, float(delta),
                                         float(tol), C.byref(em), C.c_void_p(self.stream.cuda_stream),
@@ -292,7 +295,8 @@ class Sampler:
         kt = KTimes()
         _check(self.lib.paraanya_kernel_times(self.h, C.byref(kt)))
         return {"launches": kt.launches, "eps_ms_total": kt.eps_ms_total,
-                "eps_latents": kt.eps_latents}
+                "eps_latents": kt.eps_latents, "solver_launches": kt.solver_launches,
+                "picard_ms_total": kt.picard_ms_total, "slide_ms_total": kt.slide_ms_total}
 
 
 def from_workload(wl, delta=None, *, seed_weights=None, **kw) -> "Sampler":

@@ -25,6 +25,8 @@
 // taken on fp64 sums at no bandwidth cost (these kernels are bound by memory, not by VALU).
 #include <math.h>
 
+#include <hip/hip_ext.h>
+
 #include "pa_device.h"
 
 namespace pa {
@@ -250,21 +252,21 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
 }
 
 template <bool LINEAR>
-static hipError_t launch_picard_t(const Dev& d, hipStream_t st) {
+static hipError_t launch_picard_t(const Dev& d, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const dim3 grid(d.picard_blocks, d.N), block(kThreads);
     switch (picard_tpt(d.P)) {
-        case 1: hipLaunchKernelGGL((k_picard<1, LINEAR>), grid, block, 0, st, d); break;
-        case 2: hipLaunchKernelGGL((k_picard<2, LINEAR>), grid, block, 0, st, d); break;
-        case 4: hipLaunchKernelGGL((k_picard<4, LINEAR>), grid, block, 0, st, d); break;
-        case 8: hipLaunchKernelGGL((k_picard<8, LINEAR>), grid, block, 0, st, d); break;
-        case 16: hipLaunchKernelGGL((k_picard<16, LINEAR>), grid, block, 0, st, d); break;
+        case 1: hipExtLaunchKernelGGL((k_picard<1, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 2: hipExtLaunchKernelGGL((k_picard<2, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 4: hipExtLaunchKernelGGL((k_picard<4, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 8: hipExtLaunchKernelGGL((k_picard<8, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 16: hipExtLaunchKernelGGL((k_picard<16, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_picard(const Dev& d, hipStream_t st, int linear) {
-    return linear ? launch_picard_t<true>(d, st) : launch_picard_t<false>(d, st);
+hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t e0, hipEvent_t e1) {
+    return linear ? launch_picard_t<true>(d, st, e0, e1) : launch_picard_t<false>(d, st, e0, e1);
 }
 
 // ---------------------------------------------------------------------------- slide
@@ -419,8 +421,8 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
     }
 }
 
-hipError_t launch_slide(const Dev& d, hipStream_t st) {
-    hipLaunchKernelGGL(k_slide, dim3(d.N), dim3(kSlideThreads), 0, st, d);
+hipError_t launch_slide(const Dev& d, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    hipExtLaunchKernelGGL(k_slide, dim3(d.N), dim3(kSlideThreads), 0, st, e0, e1, 0, d);
     return hipGetLastError();
 }
 

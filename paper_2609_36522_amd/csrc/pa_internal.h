@@ -62,8 +62,9 @@ struct Dev {
 
 // Kernel launchers (all asynchronous on `st`).
 hipError_t launch_reset(const Dev& d, hipStream_t st);
-hipError_t launch_slide(const Dev& d, hipStream_t st);
-hipError_t launch_picard(const Dev& d, hipStream_t st, int linear);
+// start/stop: optional events attached to the kernel's dispatch (null = untimed).
+hipError_t launch_slide(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop);
+hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_temb_table(const Dev& d, const double* t_values_dev, const __bf16* wt_dev,
                              int temb_dim, hipStream_t st);

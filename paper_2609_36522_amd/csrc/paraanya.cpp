@@ -62,8 +62,9 @@ struct paraanya {
     // profiling
     std::vector<hipEvent_t> ev_pool;
     size_t ev_used = 0;
-    int64_t prof_launches = 0;
-    double prof_ms = 0.0;
+    std::vector<int> ev_kind;         // kernel kind of each event pair
+    int64_t prof_kernel_launches[3] = {0, 0, 0};
+    double prof_kernel_ms[3] = {0.0, 0.0, 0.0};
 
     ~paraanya() {
         (void)hipStreamSynchronize(stream);
@@ -109,10 +110,25 @@ struct paraanya {
         for (size_t i = 0; i + 1 < ev_used; i += 2) {
             float ms = 0.f;
             PA_HIP(hipEventElapsedTime(&ms, ev_pool[i], ev_pool[i + 1]));
-            prof_ms += ms;
-            prof_launches += 1;
+            const int k = ev_kind[i / 2];
+            prof_kernel_ms[k] += ms;
+            prof_kernel_launches[k] += 1;
         }
         ev_used = 0;
+        ev_kind.clear();
+        return PA_OK;
+    }
+
+    // Start/stop events of one timed launch of kernel kind k (0 network, 1 Picard, 2 slide),
+    // or nulls when the handle is not profiling.
+    int timed(int k, hipEvent_t* e0, hipEvent_t* e1) {
+        *e0 = *e1 = nullptr;
+        if (!(flags & PA_FLAG_PROFILE)) return PA_OK;
+        if (k > 0 && !(flags & PA_FLAG_PROFILE_SOLVER)) return PA_OK;
+        int rc = next_event(e0);
+        if (rc) return rc;
+        if ((rc = next_event(e1))) return rc;
+        ev_kind.push_back(k);
         return PA_OK;
     }
 
@@ -129,21 +145,19 @@ struct paraanya {
 
     int enqueue_sweep() {
         // The miss list of this sweep was published by the previous k_slide (or k_reset).
+        // Under PROFILE every launch carries its own start/stop events (no marker packets
+        // between kernels).
         ctrl_fresh = false;
+        hipEvent_t e0, e1;
+        int rc;
         if (model == PA_EPS_PATCH_MLP) {
-            // Under PROFILE the network launch carries its own start/stop events (no marker
-            // packets between kernels).
-            hipEvent_t e0 = nullptr, e1 = nullptr;
-            if (flags & PA_FLAG_PROFILE) {
-                int rc = next_event(&e0);
-                if (rc) return rc;
-                rc = next_event(&e1);
-                if (rc) return rc;
-            }
+            if ((rc = timed(0, &e0, &e1))) return rc;
             PA_HIP(pa::launch_eps_mlp(d, stream, e0, e1));
         }
-        PA_HIP(pa::launch_picard(d, stream, model == PA_EPS_LINEAR));
-        PA_HIP(pa::launch_slide(d, stream));
+        if ((rc = timed(1, &e0, &e1))) return rc;
+        PA_HIP(pa::launch_picard(d, stream, model == PA_EPS_LINEAR, e0, e1));
+        if ((rc = timed(2, &e0, &e1))) return rc;
+        PA_HIP(pa::launch_slide(d, stream, e0, e1));
         return PA_OK;
     }
 };
@@ -228,7 +242,7 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
         return fail(PA_ERR_INVALID_ARG, "window must be in [1, min(T, %d)]", PA_MAX_WINDOW);
     if (!(delta >= 0.0)) return fail(PA_ERR_INVALID_ARG, "delta must be >= 0 (got %g)", delta);
     if (!(tol >= 0.0)) return fail(PA_ERR_INVALID_ARG, "tol must be >= 0 (got %g)", tol);
-    if (flags & ~(PA_FLAG_TRACE | PA_FLAG_PROFILE)) return fail(PA_ERR_INVALID_ARG, "unknown flags");
+    if (flags & ~(PA_FLAG_TRACE | PA_FLAG_PROFILE | PA_FLAG_PROFILE_SOLVER)) return fail(PA_ERR_INVALID_ARG, "unknown flags");
     const int D = (int)Dl;
     const pa_eps_model_t* em = eps_model;
     if (em->kind == PA_EPS_LINEAR) {
@@ -391,8 +405,11 @@ int paraanya_reset(paraanya_t* h, const float* x_init) {
     h->have_reset = true;
     h->host_done = false;
     h->ev_used = 0;
-    h->prof_ms = 0.0;
-    h->prof_launches = 0;
+    h->ev_kind.clear();
+    for (int k = 0; k < 3; ++k) {
+        h->prof_kernel_ms[k] = 0.0;
+        h->prof_kernel_launches[k] = 0;
+    }
     return PA_OK;
 }
 
@@ -615,8 +632,11 @@ int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out) {
     if (rc) return rc;
     rc = h->read_ctrl();
     if (rc) return rc;
-    out->launches = h->prof_launches;
-    out->eps_ms_total = h->prof_ms;
+    out->launches = h->prof_kernel_launches[0];
+    out->eps_ms_total = h->prof_kernel_ms[0];
+    out->solver_launches = h->prof_kernel_launches[1];
+    out->picard_ms_total = h->prof_kernel_ms[1];
+    out->slide_ms_total = h->prof_kernel_ms[2];
     out->eps_latents = 0;
     for (int n = 0; n < h->d.N; ++n) out->eps_latents += h->ctrl_host[n].nfe;
     return PA_OK;

@@ -67,6 +67,7 @@ def _create(shape=(1, 4, 8, 8), T=10, window=4, delta=0.05, tol=1e-3, kind=B.PA_
     (dict(tol=-1.0), "tol"),
     (dict(tol=float("nan")), "tol"),
     (dict(flags=8), "flags"),
+    (dict(flags=16), "flags"),
     (dict(null_c=True), "c is NULL"),
     (dict(kind=7), "kind"),
     (dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 4, 7, 8)), "even"),
@@ -130,7 +131,8 @@ def test_struct_layouts_match_the_header(tmp_path):
               "pa_stats_t": (B.Stats, ["nfe", "sweeps", "window_start", "nonfinite", "revisits", "revisits_below"]),
               "pa_sweep_trace_t": (B.SweepTrace, ["s", "sweep", "dev", "resid", "miss_idx", "hit"]),
               "pa_eps_model_t": (B.EpsModel, ["kind", "c", "hidden", "w1", "w3"]),
-              "pa_ktimes_t": (B.KTimes, ["launches", "eps_ms_total", "eps_latents"])}
+              "pa_ktimes_t": (B.KTimes, ["launches", "eps_ms_total", "eps_latents", "solver_launches",
+                                         "picard_ms_total", "slide_ms_total"])}
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "paraanya.h"', "int main(void) {"]
     for st, (_, fs) in fields.items():
         lines.append(f'printf("%zu\\n", sizeof({st}));')

@@ -123,6 +123,12 @@ def test_profile_counts_launches(gpu_lib):
     # sample() may enqueue a sweep or two past done; those network launches exit at once.
     assert kt["launches"] >= st["sweeps"] and kt["eps_latents"] == st["nfe"]
     assert kt["eps_ms_total"] > 0
+    assert kt["solver_launches"] == 0 and kt["picard_ms_total"] == 0.0
+    with B.from_workload(wl, profile_solver=True) as s:
+        s.sample(_x(wl))
+        kt = s.kernel_times()
+    assert kt["solver_launches"] == kt["launches"] >= st["sweeps"]
+    assert kt["picard_ms_total"] > 0 and kt["slide_ms_total"] > 0
 
 
 @pytest.mark.parametrize("T,eta", [(10, 1.0), (100, 1.0), (1000, 1.0), (50, 0.5)])
