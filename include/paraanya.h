@@ -96,7 +96,7 @@ typedef struct {
  * (sin for k < 64, cos above, frequency exp(-ln(1e4) k/64)); erf GELU; bf16 x bf16
  * products accumulated in fp32. Weights are bf16 bit patterns, row-major [in][out]:
  * w1[16][hidden], wt[temb_dim][hidden], w2[hidden][hidden], w3[hidden][16]; host memory,
- * copied at create. Supported: patch = 2, C = 4, temb_dim = 128, hidden in {512, 1024},
+ * copied at create. Supported: patch = 2, C = 4, temb_dim = 128, hidden in {512, 1024, 2048},
  * (H/2)*(W/2) a multiple of 128. */
 typedef struct {
     int32_t kind;
@@ -241,6 +241,79 @@ PA_API int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out);
 
 /* Free every resource of the handle (synchronizes its stream first). NULL-safe. */
 PA_API void paraanya_destroy(paraanya_t* h);
+
+/* ------------------------------------------------------------------ Parareal sampler
+ * The Parareal-based sampler family of Sec. 2.1 (coarse solver initializing, fine solvers
+ * refining; SRDS) with the Sec. 2.2 cache on every network evaluation, coarse or fine. The
+ * T sampling steps form B blocks of L = T / B fine DDIM steps. Coarse step of block n: one
+ * DDIM step from state nL to state (n+1)L with the network at timestep nL. Initialization:
+ * U_0 = x_init, U_{n+1} = G_n(U_n). Iteration k: fine solves of the blocks n >= k (all
+ * blocks advance one fine step per batched network launch), then U_{k+1} <- F_k and, for
+ * n = k+1..B-1 in order, U_{n+1} <- G_n(U_n) + (F_n - G_n^previous) (textbook Parareal
+ * predictor-corrector); stop when every boundary's Eq. (2) residual is <= tol, or after B
+ * iterations (then U_B equals serial fine DDIM). The cache holds one entry per fine-grid
+ * timestep; a coarse request at nL shares the entry of the first fine step of block n.
+ * Storage fp32, arithmetic fp64 with one rounding per stored value, as in the Picard
+ * sampler. Deterministic DDIM only (schedule eta must be 0). */
+#define PA_PR_MAX_BLOCKS 64
+
+typedef struct paraanya_parareal paraanya_parareal_t;
+
+typedef struct {
+    int64_t nfe;          /* network evaluations (cache misses) */
+    int64_t hits;         /* requests served from the cache */
+    int64_t requests;     /* nfe + hits */
+    int32_t iterations;   /* Parareal iterations after the initialization */
+    int32_t done;
+    int32_t nonfinite;    /* a boundary residual was NaN/Inf */
+    int32_t pad;
+} pa_parareal_stats_t;
+
+/* One network request (test hook). Requests are numbered in issue order: the B coarse
+ * requests of the initialization, then per iteration the fine steps (blocks k..B-1 each)
+ * and the coarse requests of blocks k+1..B-1. */
+typedef struct {
+    int32_t iteration;    /* -1 for the initialization */
+    int32_t phase;        /* 0 initialization, 1 fine step, 2 coarse correction */
+    int32_t t;            /* fine-grid timestep */
+    int32_t block;
+    int32_t hit;          /* Eq. (5) */
+    int32_t pad;
+    double  dev;          /* Eq. (4) (fp64 sum); NaN without a cache entry */
+} pa_request_trace_t;
+
+/* Create a Parareal sampler. latent_shape = {1, C, H, W}; blocks in [1, PA_PR_MAX_BLOCKS]
+ * dividing T; delta, tol as for paraanya_create; flags: PA_FLAG_TRACE (request records,
+ * fresh outputs and boundary residuals), PA_FLAG_PROFILE (network launch timings).
+ * Errors: INVALID_ARG, UNSUPPORTED (eta != 0, model shape not built), OOM, HIP. */
+PA_API int paraanya_parareal_create(const int32_t latent_shape[4], int32_t T,
+                                    const pa_schedule_t* schedule, int32_t blocks, double delta,
+                                    double tol, const pa_eps_model_t* eps_model, void* stream,
+                                    uint32_t flags, paraanya_parareal_t** out);
+
+/* One full sample: initialization and iterations until done; x_init, x_out device D fp32
+ * (may alias); returns after x_out is written. NONFINITE if a residual was NaN/Inf. */
+PA_API int paraanya_parareal_sample(paraanya_parareal_t* h, const float* x_init, float* x_out);
+
+/* Counters of the last sample; STATE before the first. */
+PA_API int paraanya_parareal_stats(paraanya_parareal_t* h, pa_parareal_stats_t* out);
+
+/* Test hook (PA_FLAG_TRACE): request i of the last sample; eps (host, D fp32, may be NULL)
+ * receives its fresh network output when it was a miss. INVALID_ARG for i out of range. */
+PA_API int paraanya_parareal_trace(paraanya_parareal_t* h, int32_t i, pa_request_trace_t* out,
+                                   float* eps);
+
+/* Test hook (PA_FLAG_TRACE): boundary residuals r[0..B] of iteration k (entries 0..k are 0). */
+PA_API int paraanya_parareal_residuals(paraanya_parareal_t* h, int32_t k, double* r);
+
+/* Test hook: the boundary states U_0..U_B of the last sample, host (B+1) x D fp32. */
+PA_API int paraanya_parareal_read_boundaries(paraanya_parareal_t* h, float* U);
+
+/* Network-launch timings of the last sample (PA_FLAG_PROFILE); STATE without it. */
+PA_API int paraanya_parareal_kernel_times(paraanya_parareal_t* h, pa_ktimes_t* out);
+
+/* Free the handle (synchronizes its stream first). NULL-safe. */
+PA_API void paraanya_parareal_destroy(paraanya_parareal_t* h);
 
 /* Thread-local message of the last failing call on this thread ("" if none). */
 PA_API const char* paraanya_last_error(void);

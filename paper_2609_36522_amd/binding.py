@@ -23,6 +23,7 @@ PA_ERR_NONFINITE = -5
 PA_ERR_UNSUPPORTED = -6
 PA_MAX_WINDOW = 256
 PA_MAX_BATCH = 64
+PA_PR_MAX_BLOCKS = 64
 
 PA_SCHED_SCALED_LINEAR = 0
 PA_SCHED_EXPLICIT = 1
@@ -37,7 +38,11 @@ EXPORTED = ("paraanya_create", "paraanya_reset", "paraanya_sweep", "paraanya_sam
             "paraanya_stats", "paraanya_trace", "paraanya_read_state", "paraanya_coefficients",
             "paraanya_kernel_times", "paraanya_destroy", "paraanya_last_error",
             "paraanya_status_str", "paraanya_set_noise", "paraanya_set_revisit_threshold",
-            "paraanya_stats_sample", "paraanya_trace_sample", "paraanya_read_state_sample")
+            "paraanya_stats_sample", "paraanya_trace_sample", "paraanya_read_state_sample",
+            "paraanya_parareal_create", "paraanya_parareal_sample", "paraanya_parareal_stats",
+            "paraanya_parareal_trace", "paraanya_parareal_residuals",
+            "paraanya_parareal_read_boundaries", "paraanya_parareal_kernel_times",
+            "paraanya_parareal_destroy")
 
 
 class Schedule(C.Structure):
@@ -86,6 +91,21 @@ class KTimes(C.Structure):
                 ("picard_ms_total", C.c_double), ("slide_ms_total", C.c_double)]
 
 
+class PrStats(C.Structure):
+    _fields_ = [("nfe", C.c_int64), ("hits", C.c_int64), ("requests", C.c_int64),
+                ("iterations", C.c_int32), ("done", C.c_int32), ("nonfinite", C.c_int32),
+                ("pad", C.c_int32)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_ if k != "pad"}
+
+
+class RequestTrace(C.Structure):
+    _fields_ = [("iteration", C.c_int32), ("phase", C.c_int32), ("t", C.c_int32),
+                ("block", C.c_int32), ("hit", C.c_int32), ("pad", C.c_int32),
+                ("dev", C.c_double)]
+
+
 _LIB = None
 
 
@@ -115,11 +135,22 @@ def load_library(path: str = LIB_PATH):
     lib.paraanya_kernel_times.argtypes = [P, C.POINTER(KTimes)]
     lib.paraanya_destroy.argtypes = [P]
     lib.paraanya_destroy.restype = None
+    lib.paraanya_parareal_create.argtypes = [C.POINTER(C.c_int32), I32, C.POINTER(Schedule), I32, F64,
+                                             F64, C.POINTER(EpsModel), V, C.c_uint32, C.POINTER(P)]
+    lib.paraanya_parareal_sample.argtypes = [P, P, P]
+    lib.paraanya_parareal_stats.argtypes = [P, C.POINTER(PrStats)]
+    lib.paraanya_parareal_trace.argtypes = [P, I32, C.POINTER(RequestTrace), P]
+    lib.paraanya_parareal_residuals.argtypes = [P, I32, P]
+    lib.paraanya_parareal_read_boundaries.argtypes = [P, P]
+    lib.paraanya_parareal_kernel_times.argtypes = [P, C.POINTER(KTimes)]
+    lib.paraanya_parareal_destroy.argtypes = [P]
+    lib.paraanya_parareal_destroy.restype = None
     lib.paraanya_last_error.restype = C.c_char_p
     lib.paraanya_status_str.argtypes = [C.c_int]
     lib.paraanya_status_str.restype = C.c_char_p
     for name in EXPORTED:
-        if name not in ("paraanya_destroy", "paraanya_last_error", "paraanya_status_str"):
+        if name not in ("paraanya_destroy", "paraanya_last_error", "paraanya_status_str",
+                        "paraanya_parareal_destroy"):
             getattr(lib, name).restype = C.c_int
     _LIB = lib
     return lib
@@ -144,6 +175,32 @@ def _ptr(a: np.ndarray, ctype):
     return a.ctypes.data_as(C.POINTER(ctype))
 
 
+def _schedule_and_model(keep, schedule, eta, model, c, weights, hidden):
+    """ctypes Schedule and EpsModel; arrays they point to are appended to ``keep``."""
+    if schedule is None:
+        sc = Schedule(PA_SCHED_SCALED_LINEAR, 0.00085, 0.012, 1000, PA_SPACING_TRAILING, 1,
+                      None, None, float(eta))
+    else:
+        ab = np.ascontiguousarray(schedule["alpha_bar"], dtype=np.float64)
+        tv = np.ascontiguousarray(schedule["t_values"], dtype=np.int32)
+        keep += [ab, tv]
+        sc = Schedule(PA_SCHED_EXPLICIT, 0.0, 0.0, 0, 0, 0, _ptr(ab, C.c_double),
+                      _ptr(tv, C.c_int32), float(eta))
+    if model == "linear":
+        cc = np.ascontiguousarray(c, dtype=np.float32)
+        keep.append(cc)
+        em = EpsModel(PA_EPS_LINEAR, _ptr(cc, C.c_float), 0, 0, 0, None, None, None, None)
+    elif model == "patch_mlp":
+        ws = {k: np.ascontiguousarray(weights[k], dtype=np.uint16) for k in ("w1", "wt", "w2", "w3")}
+        keep.append(ws)
+        em = EpsModel(PA_EPS_PATCH_MLP, None, 2, int(hidden), int(ws["wt"].shape[0]),
+                      _ptr(ws["w1"], C.c_uint16), _ptr(ws["wt"], C.c_uint16),
+                      _ptr(ws["w2"], C.c_uint16), _ptr(ws["w3"], C.c_uint16))
+    else:
+        raise ValueError(f"unknown model {model!r}")
+    return sc, em
+
+
 class Sampler:
     """One handle of the cached Picard sampler.
 
@@ -166,27 +223,7 @@ class Sampler:
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         shape = (C.c_int32 * 4)(self.N, *self.latent)
         self._keep = []
-        if schedule is None:
-            sc = Schedule(PA_SCHED_SCALED_LINEAR, 0.00085, 0.012, 1000, PA_SPACING_TRAILING, 1,
-                          None, None, float(eta))
-        else:
-            ab = np.ascontiguousarray(schedule["alpha_bar"], dtype=np.float64)
-            tv = np.ascontiguousarray(schedule["t_values"], dtype=np.int32)
-            self._keep += [ab, tv]
-            sc = Schedule(PA_SCHED_EXPLICIT, 0.0, 0.0, 0, 0, 0, _ptr(ab, C.c_double),
-                          _ptr(tv, C.c_int32), float(eta))
-        if model == "linear":
-            cc = np.ascontiguousarray(c, dtype=np.float32)
-            self._keep.append(cc)
-            em = EpsModel(PA_EPS_LINEAR, _ptr(cc, C.c_float), 0, 0, 0, None, None, None, None)
-        elif model == "patch_mlp":
-            ws = {k: np.ascontiguousarray(weights[k], dtype=np.uint16) for k in ("w1", "wt", "w2", "w3")}
-            self._keep.append(ws)
-            em = EpsModel(PA_EPS_PATCH_MLP, None, 2, int(hidden), int(ws["wt"].shape[0]),
-                          _ptr(ws["w1"], C.c_uint16), _ptr(ws["wt"], C.c_uint16),
-                          _ptr(ws["w2"], C.c_uint16), _ptr(ws["w3"], C.c_uint16))
-        else:
-            raise ValueError(f"unknown model {model!r}")
+        sc, em = _schedule_and_model(self._keep, schedule, eta, model, c, weights, hidden)
         flags = (PA_FLAG_TRACE if trace else 0) | (PA_FLAG_PROFILE if profile else 0) | \
             (PA_FLAG_PROFILE | PA_FLAG_PROFILE_SOLVER if profile_solver else 0)
         h = C.c_void_p()
@@ -310,3 +347,99 @@ def from_workload(wl, delta=None, *, seed_weights=None, **kw) -> "Sampler":
     return Sampler(wl.latent, wl.T, wl.window, d, wl.tol, "patch_mlp", weights=w,
                    hidden=wl.hidden, **kw)
 
+
+
+class Parareal:
+    """One handle of the cached Parareal sampler (T steps in ``blocks`` blocks)."""
+
+    def __init__(self, latent, T, blocks, delta, tol, model, *, c=None, weights=None, hidden=0,
+                 schedule=None, stream=None, trace=False, profile=False):
+        import torch
+        self.lib = load_library()
+        self.latent = tuple(int(v) for v in latent)
+        self.T, self.B = int(T), int(blocks)
+        self.D = int(np.prod(self.latent))
+        self.torch = torch
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        self._keep = []
+        sc, em = _schedule_and_model(self._keep, schedule, 0.0, model, c, weights, hidden)
+        shape = (C.c_int32 * 4)(1, *self.latent)
+        flags = (PA_FLAG_TRACE if trace else 0) | (PA_FLAG_PROFILE if profile else 0)
+        h = C.c_void_p()
+        _check(self.lib.paraanya_parareal_create(shape, self.T, C.byref(sc), self.B, float(delta),
+                                                 float(tol), C.byref(em),
+                                                 C.c_void_p(self.stream.cuda_stream), flags, C.byref(h)))
+        self.h = h
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.paraanya_parareal_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def _dev(self, x):
+        t = self.torch
+        if not (isinstance(x, t.Tensor) and x.is_cuda and x.dtype == t.float32 and x.is_contiguous()
+                and x.numel() == self.D):
+            raise ValueError(f"expected a contiguous fp32 CUDA tensor of {self.D} elements")
+        return C.c_void_p(x.data_ptr())
+
+    def sample(self, x_init, x_out=None):
+        if x_out is None:
+            x_out = self.torch.empty_like(x_init)
+        _check(self.lib.paraanya_parareal_sample(self.h, self._dev(x_init), self._dev(x_out)))
+        return x_out
+
+    def stats(self) -> dict:
+        st = PrStats()
+        _check(self.lib.paraanya_parareal_stats(self.h, C.byref(st)))
+        return st.as_dict()
+
+    def trace(self, i: int, with_eps: bool = False):
+        """(record dict, fresh output or None) of request i of the last sample."""
+        r = RequestTrace()
+        eps = np.empty(self.D, np.float32) if with_eps else None
+        _check(self.lib.paraanya_parareal_trace(self.h, int(i), C.byref(r),
+                                                None if eps is None else eps.ctypes.data_as(C.c_void_p)))
+        rec = {"iteration": r.iteration, "phase": r.phase, "t": r.t, "block": r.block,
+               "hit": bool(r.hit), "dev": r.dev}
+        return rec, (eps if (with_eps and not r.hit) else None)
+
+    def residuals(self, k: int) -> np.ndarray:
+        r = np.empty(self.B + 1, np.float64)
+        _check(self.lib.paraanya_parareal_residuals(self.h, int(k), r.ctypes.data_as(C.c_void_p)))
+        return r
+
+    def boundaries(self) -> np.ndarray:
+        U = np.empty((self.B + 1, self.D), np.float32)
+        _check(self.lib.paraanya_parareal_read_boundaries(self.h, U.ctypes.data_as(C.c_void_p)))
+        return U
+
+    def kernel_times(self) -> dict:
+        kt = KTimes()
+        _check(self.lib.paraanya_parareal_kernel_times(self.h, C.byref(kt)))
+        return {"launches": kt.launches, "eps_ms_total": kt.eps_ms_total,
+                "eps_latents": kt.eps_latents}
+
+
+def parareal_from_workload(wl, delta=None, *, seed_weights=None, **kw) -> "Parareal":
+    """Parareal handle for a workload with ``wl.blocks`` blocks and its seeded inputs."""
+    from . import inputs
+    d = wl.delta if delta is None else delta
+    if wl.model == "linear":
+        return Parareal(wl.latent, wl.T, wl.blocks, d, wl.tol, "linear",
+                        c=inputs.linear_coefficients(wl.T), **kw)
+    w = inputs.mlp_weights(wl.hidden, temb_dim=wl.temb_dim) if seed_weights is None else seed_weights
+    return Parareal(wl.latent, wl.T, wl.blocks, d, wl.tol, "patch_mlp", weights=w,
+                    hidden=wl.hidden, **kw)

@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libparaanya.so")
 
-SOURCES = ["paraanya.cpp", "k_solver.hip", "k_epsnet.hip"]
+SOURCES = ["paraanya.cpp", "paraanya_parareal.cpp", "host_common.cpp", "k_solver.hip", "k_epsnet.hip", "k_parareal.hip"]
 ARCH = "gfx950"
 
 

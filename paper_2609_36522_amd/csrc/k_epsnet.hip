@@ -287,7 +287,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     }
 }
 
-int mlp_supported(int hidden) { return hidden == 512 || hidden == 1024; }
+int mlp_supported(int hidden) { return hidden == 512 || hidden == 1024 || hidden == 2048; }
 
 int mlp_tokens_per_item() { return kTok; }
 
@@ -302,6 +302,9 @@ hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEve
             break;
         case 1024:
             hipExtLaunchKernelGGL(k_eps_mlp<1024>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, start, stop, 0, d);
+            break;
+        case 2048:
+            hipExtLaunchKernelGGL(k_eps_mlp<2048>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, start, stop, 0, d);
             break;
         default:
             return hipErrorInvalidValue;

@@ -58,6 +58,12 @@ struct Dev {
     int32_t nsplit;            // halves of the output units (partials summed by k_picard)
     int32_t picard_blocks;
     int32_t mlp_grid;
+    // Parareal sampler only (k_parareal.hip)
+    float* Gc;                         // [B][D] stored coarse values G_n
+    double* pr_coef;                   // [B][2] coarse step (ac_n, bc_n)
+    pa_request_trace_t* trace_pr;      // request records or null
+    float* trace_eps;                  // [records][D] fresh outputs of the misses, or null
+    double* trace_res;                 // [B][B+1] boundary residuals per iteration, or null
 };
 
 // Kernel launchers (all asynchronous on `st`).

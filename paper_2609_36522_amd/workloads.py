@@ -23,6 +23,7 @@ class Workload:
     hidden: int = 0        # patch-MLP hidden width H
     temb_dim: int = 128
     patch: int = 2
+    blocks: int = 0        # Parareal blocks (0: the Picard sampler's workload)
 
     @property
     def D(self) -> int:
@@ -50,6 +51,11 @@ SD_MLP = Workload("mlp_4x64x64_T100_P32_H1024", (4, 64, 64), 100, 32, 0.05, 1e-3
 LONG_MLP = Workload("mlp_4x64x64_T1000_P128_H1024", (4, 64, 64), 1000, 128, 0.05, 1e-3,
                     "patch_mlp", hidden=1024)
 
+# Parareal-style variant: 4x96x96 latent, T=100 in 10 blocks of 10 fine steps, H=2048 over
+# 2304 tokens, fine and coarse outputs cached at delta=0.05.
+PARAREAL_MLP = Workload("parareal_4x96x96_T100_B10_H2048", (4, 96, 96), 100, 1, 0.05, 1e-3,
+                        "patch_mlp", hidden=2048, blocks=10)
+
 HEADLINE_DELTAS = (0.0, 0.02, 0.05, 0.1)
 
-ALL = {w.name: w for w in (TINY_LINEAR, SMALL_MLP, SD_MLP, LONG_MLP)}
+ALL = {w.name: w for w in (TINY_LINEAR, SMALL_MLP, SD_MLP, LONG_MLP, PARAREAL_MLP)}

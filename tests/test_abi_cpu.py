@@ -22,7 +22,7 @@ def _declared():
 def test_library_exports_every_declared_symbol():
     lib = B.load_library()
     names = _declared()
-    assert len(names) == 17
+    assert len(names) == 25
     assert sorted(B.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -132,7 +132,9 @@ def test_struct_layouts_match_the_header(tmp_path):
               "pa_sweep_trace_t": (B.SweepTrace, ["s", "sweep", "dev", "resid", "miss_idx", "hit"]),
               "pa_eps_model_t": (B.EpsModel, ["kind", "c", "hidden", "w1", "w3"]),
               "pa_ktimes_t": (B.KTimes, ["launches", "eps_ms_total", "eps_latents", "solver_launches",
-                                         "picard_ms_total", "slide_ms_total"])}
+                                         "picard_ms_total", "slide_ms_total"]),
+              "pa_parareal_stats_t": (B.PrStats, ["nfe", "hits", "requests", "iterations", "done", "nonfinite"]),
+              "pa_request_trace_t": (B.RequestTrace, ["iteration", "phase", "t", "block", "hit", "dev"])}
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "paraanya.h"', "int main(void) {"]
     for st, (_, fs) in fields.items():
         lines.append(f'printf("%zu\\n", sizeof({st}));')
@@ -149,3 +151,47 @@ def test_struct_layouts_match_the_header(tmp_path):
         assert next(it) == C.sizeof(cls), st
         for f in fs:
             assert next(it) == getattr(cls, f).offset, f"{st}.{f}"
+
+
+def _pr_create(shape=(1, 4, 8, 8), T=20, blocks=4, delta=0.05, tol=1e-3, eta=0.0, flags=0,
+               kind=B.PA_EPS_LINEAR):
+    lib = B.load_library()
+    sh = (C.c_int32 * 4)(*shape)
+    sc = B.Schedule(B.PA_SCHED_SCALED_LINEAR, 0.00085, 0.012, 1000, 0, 1, None, None, eta)
+    c = np.ones(max(T, 1), np.float32)
+    w = {k: np.zeros(1, np.uint16) for k in ("w1", "wt", "w2", "w3")}
+    em = B.EpsModel(kind, c.ctypes.data_as(C.POINTER(C.c_float)), 2, 1024, 128,
+                    *(w[k].ctypes.data_as(C.POINTER(C.c_uint16)) for k in ("w1", "wt", "w2", "w3")))
+    h = C.c_void_p(1234)
+    rc = lib.paraanya_parareal_create(sh, T, C.byref(sc), blocks, delta, tol, C.byref(em), None,
+                                      flags, C.byref(h))
+    return rc, h.value, lib.paraanya_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,code,frag", [
+    (dict(shape=(2, 4, 8, 8)), B.PA_ERR_INVALID_ARG, "batch"),
+    (dict(blocks=3), B.PA_ERR_INVALID_ARG, "blocks"),
+    (dict(blocks=0), B.PA_ERR_INVALID_ARG, "blocks"),
+    (dict(T=130, blocks=65), B.PA_ERR_INVALID_ARG, "blocks"),
+    (dict(delta=-1.0), B.PA_ERR_INVALID_ARG, "delta"),
+    (dict(tol=float("nan")), B.PA_ERR_INVALID_ARG, "tol"),
+    (dict(flags=4), B.PA_ERR_INVALID_ARG, "flags"),
+    (dict(eta=1.0), B.PA_ERR_UNSUPPORTED, "eta"),
+    (dict(kind=B.PA_EPS_PATCH_MLP, shape=(1, 4, 16, 16)), B.PA_ERR_UNSUPPORTED, "token"),
+])
+def test_parareal_create_rejects(kw, code, frag):
+    rc, h, msg = _pr_create(**kw)
+    assert rc == code, msg
+    assert h is None and frag in msg
+
+
+def test_parareal_null_handle_calls_fail_cleanly():
+    lib = B.load_library()
+    assert lib.paraanya_parareal_sample(None, None, None) == B.PA_ERR_INVALID_ARG
+    st = B.PrStats()
+    assert lib.paraanya_parareal_stats(None, C.byref(st)) == B.PA_ERR_INVALID_ARG
+    r = B.RequestTrace()
+    assert lib.paraanya_parareal_trace(None, 0, C.byref(r), None) == B.PA_ERR_INVALID_ARG
+    assert lib.paraanya_parareal_residuals(None, 0, None) == B.PA_ERR_INVALID_ARG
+    assert lib.paraanya_parareal_read_boundaries(None, None) == B.PA_ERR_INVALID_ARG
+    lib.paraanya_parareal_destroy(None)
