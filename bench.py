@@ -15,6 +15,8 @@ Beside the headline line (same JSON object, extra keys):
                      sweep serves every sample's misses): samples/s, eps evals/s;
   ddpm_window64      ancestral DDPM (eta = 1, pre-drawn step noise) over T = 1000 with a
                      window of 64 on the same latent and network, delta in {0, 0.05}.
+  parareal           the Parareal-style cached sampler: 4x96x96 latent, T = 100 in 10 blocks,
+                     patch-MLP H = 2048 over 2304 tokens, delta in {0, 0.05}.
 
 Prints one JSON line (rank 0). The roofline object describes the dominant kernel (the fused
 patch-MLP network kernel): achieved = algorithmic FLOPs of its launches / their summed
@@ -110,6 +112,33 @@ def timed_samples(sampler, x, steps, warmup, torch):
             "launches": launches, "revisits": revisits, "revisits_below": below,
             "picard_ms": picard_ms, "slide_ms": slide_ms, "solver_launches": solver_launches,
             "out": out}
+
+
+def parareal_case(wl, delta, steps, warmup, torch, weights):
+    """Timed Parareal samples (profiled handle: events on the network launches)."""
+    from paper_2609_36522_amd import binding, inputs
+    x = torch.from_numpy(inputs.x_init(wl.latent).reshape(-1)).cuda()
+    out = torch.empty_like(x)
+    with binding.parareal_from_workload(wl, delta, seed_weights=weights, profile=True) as s:
+        for _ in range(warmup):
+            s.sample(x, out)
+        torch.cuda.synchronize()
+        nfe = hits = iters = launches = 0
+        eps_ms = 0.0
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            s.sample(x, out)
+            st = s.stats()
+            kt = s.kernel_times()
+            nfe += st["nfe"]
+            hits += st["hits"]
+            iters += st["iterations"]
+            eps_ms += kt["eps_ms_total"]
+            launches += kt["launches"]
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+    return {"seconds": dt, "nfe": nfe, "hits": hits, "iters": iters, "eps_ms": eps_ms,
+            "launches": launches}
 
 
 def solver_kernels(r, D):
@@ -243,6 +272,30 @@ def main():
                                    "sweeps_per_sample": r["sweeps"] / dsteps}
                           for d, r in dd.items()},
             "nfe_saved_vs_delta0": 1.0 - dd[PRIMARY_DELTA]["nfe"] / dd[0.0]["nfe"]}
+        # the Parareal-style cached sampler
+        wp = workloads.PARAREAL_MLP
+        wts = inputs.mlp_weights(wp.hidden, temb_dim=wp.temb_dim)
+        fpp = flops_per_eval(wp)
+        psteps = max(args.steps // 10, 3)
+        pp = {}
+        for d in (0.0, PRIMARY_DELTA):
+            r = parareal_case(wp, d, psteps, 1, torch, wts)
+            pp[d] = r
+            print(f"[bench] parareal delta={d}: {1e3 * r['seconds'] / psteps:.3f} ms/sample, "
+                  f"NFE {r['nfe'] / psteps:.0f}, {r['iters'] / psteps:.1f} iterations",
+                  file=sys.stderr, flush=True)
+        extras["parareal"] = {
+            "workload": wp.name, "latent": list(wp.latent), "T": wp.T, "blocks": wp.blocks,
+            "hidden": wp.hidden, "tokens": wp.tokens, "gflop_per_eval": fpp / 1e9, "steps": psteps,
+            "per_delta": {str(d): {"ms_per_sample": 1e3 * r["seconds"] / psteps,
+                                   "eps_evals_per_s": r["nfe"] / r["seconds"],
+                                   "nfe_per_sample": r["nfe"] / psteps,
+                                   "hits_per_sample": r["hits"] / psteps,
+                                   "iterations_per_sample": r["iters"] / psteps,
+                                   "eps_kernel_tflops": (r["nfe"] * fpp) / (r["eps_ms"] * 1e-3) / 1e12
+                                   if r["eps_ms"] > 0 else None}
+                          for d, r in pp.items()},
+            "nfe_saved_vs_delta0": 1.0 - pp[PRIMARY_DELTA]["nfe"] / pp[0.0]["nfe"]}
 
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * (1 << 20) // 4
