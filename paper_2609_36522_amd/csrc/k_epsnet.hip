@@ -27,6 +27,8 @@
 // use the same lane->slot convention, so any consistent slot->k assignment is valid.
 #include <math.h>
 
+#include <type_traits>
+
 #include <hip/hip_ext.h>
 
 #include "pa_device.h"
@@ -45,6 +47,7 @@ constexpr int kKC = 256;                // h1 units per LDS buffer (K-chunk); tw
 constexpr int kWaves = 8;               // wave w owns output units [64w, 64w + 64) of the item
 constexpr int kFeat = 16;               // 2x2 patch x 4 channels
 constexpr int kXRow = kFeat + 8;        // padded LDS row of the token tile (bf16)
+constexpr int kInterleave = 0;          // VALU instructions scheduled after each GEMM2 MFMA (0: free)
 
 // erf-GELU, x * Phi(x) = max(x, 0) - a Q(a) with a = |x| and Q the normal upper tail,
 // branch-free. Q(a) = 2^(-P(min(a, 5))) with P a degree-7 polynomial fitted toward the
@@ -103,6 +106,10 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     // h1 chunks, double-buffered: chunk c + 1 is computed while GEMM2 consumes chunk c.
     __shared__ __attribute__((aligned(16))) __bf16 h1s[2][kTok * HRow];
     __shared__ __attribute__((aligned(16))) __bf16 xs[kTok * kXRow];
+    // e_t of the item's timestep. Read from LDS in the GELU slices: a global load there
+    // would share the in-order vector-memory counter with the W2 prefetch, and waiting for
+    // it would wait for the prefetched fragments too.
+    __shared__ __attribute__((aligned(16))) float es[H];
     float* red = reinterpret_cast<float*>(&h1s[0][0]);   // [kWaves][kTok][16] after GEMM2
     static_assert(kWaves * kTok * kFeat * 4 <= 2 * kTok * HRow * 2, "reduction buffer must fit");
 
@@ -142,21 +149,23 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         const float* et = d.temb + (size_t)t * H;
         const int hb0 = ns * (kNH / 32) + w * 2;   // this wave's first 32-unit block of W2^T
 
-        // ---- 0. gather + patchify + bf16
+        // ---- 0. gather + patchify + bf16; e_t into LDS
         for (int e = tid; e < kTok * kFeat; e += NT) {
             const TokPos p = tok_pos(e, tb, d.Himg, d.Wimg);
             xs[p.tl * kXRow + p.f] = (__bf16)xt[p.idx];
         }
+        for (int i = tid; i < H / 4; i += NT)
+            reinterpret_cast<float4*>(es)[i] = reinterpret_cast<const float4*>(et)[i];
         __syncthreads();
 
         // ---- 1. h1 = GELU(x W1 + e_t): wave w computes units [32w, 32w + 32) of a chunk,
         // one 32-token slice per call, into LDS rows [token][unit].
         bf16x8 w1a;
-        const float* ek = et;                // e_t of the chunk's units (read where used)
+        const float* ek = es;                // e_t of the chunk's units (LDS)
         auto h1_setup = [&](int kc) {
             const int n0 = kc * kKC + w * 32;
             w1a = *reinterpret_cast<const bf16x8*>(d.w1t + (size_t)(n0 + l32) * kFeat + g * 8);
-            ek = et + n0 + g * 4;
+            ek = es + n0 + g * 4;
         };
         f32x16 h1acc;
         auto h1_mfma = [&](int tb4) {
@@ -192,59 +201,82 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
 #pragma unroll
             for (int tb4 = 0; tb4 < 4; ++tb4) acc2[hb][tb4] = zero16;
 
-        for (int kc = 0; kc < KCH; ++kc) {
-            // ---- 2. acc2 += W2^T h1^T over chunk kc (two register stages of W2^T fragments),
-            // with chunk kc + 1's h1 slices computed in between (the other wave of the SIMD
-            // can issue VALU while this one waits on the matrix core). A wave raises its issue
-            // priority while it feeds MFMA groups: the two waves of a SIMD then drift out of
-            // step, one in its MFMA group while the other is in its GELU slice (measured: 12%
-            // faster at 25 misses; without it both run their MFMA and VALU phases together).
-            const bool more = kc + 1 < KCH;
-            if (more) h1_setup(kc + 1);
-            __bf16* nbuf = h1s[(kc + 1) & 1];
+        // W2^T fragments of k-block kb of chunk kc, for this wave's two 32-unit blocks.
+        auto load_a = [&](bf16x8 (&A)[2][2], int kc, int kb) {
             const bf16x8* wa = w2lane + ((size_t)hb0 * KS + kc * (kKC / 16)) * 64;
-            const __bf16* h1b = h1s[kc & 1] + l32 * HRow + g * 8;
-            bf16x8 A0[2][2], A1[2][2];
-            auto load_a = [&](bf16x8 (&A)[2][2], int kb) {
 #pragma unroll
-                for (int hb = 0; hb < 2; ++hb)
+            for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
-                    for (int j = 0; j < 2; ++j) A[hb][j] = wa[((size_t)hb * KS + 2 * kb + j) * 64];
-            };
-            auto mma = [&](const bf16x8 (&A)[2][2], int kb) {
+                for (int j = 0; j < 2; ++j) A[hb][j] = wa[((size_t)hb * KS + 2 * kb + j) * 64];
+        };
+        bf16x8 A0[2][2], A1[2][2];
+        // GEMM2 MFMA group of k-block kb: 16 MFMAs over the four 32-token slices; the B
+        // operands (h1^T from LDS) of slice tb4 + 1 are read while slice tb4 multiplies.
+        auto mma = [&](const bf16x8 (&A)[2][2], const __bf16* h1b, int kb) {
+            bf16x8 B[2][2];
 #pragma unroll
-                for (int tb4 = 0; tb4 < 4; ++tb4) {
-                    bf16x8 B[2];
+            for (int j = 0; j < 2; ++j) B[0][j] = *reinterpret_cast<const bf16x8*>(h1b + kb * 32 + j * 16);
+#pragma unroll
+            for (int tb4 = 0; tb4 < 4; ++tb4) {
+                if (tb4 + 1 < 4) {
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
-                        B[j] = *reinterpret_cast<const bf16x8*>(h1b + tb4 * 32 * HRow + kb * 32 + j * 16);
-#pragma unroll
-                    for (int j = 0; j < 2; ++j)
-#pragma unroll
-                        for (int hb = 0; hb < 2; ++hb)
-                            acc2[hb][tb4] = mfma32(A[hb][j], B[j], acc2[hb][tb4]);
+                        B[(tb4 + 1) & 1][j] = *reinterpret_cast<const bf16x8*>(
+                            h1b + (tb4 + 1) * 32 * HRow + kb * 32 + j * 16);
                 }
-            };
-            load_a(A0, 0);
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int hb = 0; hb < 2; ++hb)
+                        acc2[hb][tb4] = mfma32(A[hb][j], B[tb4 & 1][j], acc2[hb][tb4]);
+            }
+        };
+        // One chunk of GEMM2 (two register stages of W2^T fragments, the stream running on
+        // across chunk boundaries). MORE: chunk kc + 1 exists; its h1 slices are computed
+        // between the MFMA groups (same basic block, so the VALU work of the GELU can be
+        // interleaved with the MFMAs: kInterleave VALU instructions per MFMA). A wave raises
+        // its issue priority while it feeds MFMA groups, so that the two waves of a SIMD
+        // drift out of step (one in its MFMA group while the other is in its GELU slice).
+        auto chunk = [&](int kc, auto more_c) {
+            constexpr bool more = decltype(more_c)::value;
+            if constexpr (more) h1_setup(kc + 1);
+            __bf16* nbuf = h1s[(kc + 1) & 1];
+            const __bf16* h1b = h1s[kc & 1] + l32 * HRow + g * 8;
 #pragma unroll
             for (int it = 0; it < ITER; ++it) {
                 const int kb = 2 * it;
-                load_a(A1, kb + 1);
+                load_a(A1, kc, kb + 1);
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(1);
-                mma(A0, kb);
+                mma(A0, h1b, kb);
+                if constexpr (more) {
+                    h1_slice(nbuf, it);
+                    if constexpr (kInterleave > 0) {
+#pragma unroll
+                        for (int q = 0; q < 17; ++q) {
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                            __builtin_amdgcn_sched_group_barrier(0x002, kInterleave, 0);
+                        }
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(0);
-                if (more) h1_slice(nbuf, it);
-                __builtin_amdgcn_sched_barrier(0);
-                load_a(A0, kb + 2 < KBC ? kb + 2 : KBC - 1);
+                // Next fragments: this chunk's, or the first of the next chunk (after the
+                // last chunk an unused reload of chunk 0, kept unconditional so the wait for
+                // A1 below counts exactly these four loads as younger).
+                if (kb + 2 < KBC) load_a(A0, kc, kb + 2);
+                else load_a(A0, more ? kc + 1 : 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(1);
-                mma(A1, kb + 1);
+                mma(A1, h1b, kb + 1);
                 __builtin_amdgcn_s_setprio(0);
                 __builtin_amdgcn_sched_barrier(0);
             }
             __syncthreads();                 // chunk kc + 1 complete; chunk kc's buffer free
-        }
+        };
+        load_a(A0, 0, 0);
+        for (int kc = 0; kc + 1 < KCH; ++kc) chunk(kc, std::true_type{});
+        chunk(KCH - 1, std::false_type{});
 
         // ---- 3. eps^T partial = W3p GELU(h2^T) straight from the accumulators
         f32x16 acc3[4] = {zero16, zero16, zero16, zero16};
