@@ -169,3 +169,11 @@ def test_batch_latents_are_distinct_seeds():
     for n in range(3):
         assert np.array_equal(xb[n], inputs.x_init((4, 8, 8), inputs.SEED_BATCH_BASE + n))
     assert not np.array_equal(xb[0], xb[1])
+
+
+def test_revisit_threshold_is_strict():
+    """'Below the threshold' is strict; first entries (NaN) are no revisits."""
+    nan = float("nan")
+    trace = [{"dev": [nan, nan]}, {"dev": [0.05, 0.04, nan]}, {"dev": [0.0, 0.0500001]}]
+    assert sp.revisit_counts(trace, 0.05) == (7, 4, 2)
+    assert sp.revisit_counts(trace, 0.0) == (7, 4, 0)

@@ -61,6 +61,8 @@ def test_full_iterations_give_serial_fine_ddim(model):
     out, tr, st = pr.sample(x, T, B, 0.0, -1.0, ab, alpha, b, eps)   # never converged early
     assert st["iters"] == B
     assert np.array_equal(out, serial)
+    # the iteration ends itself after B iterations (exactness), flagged as done
+    assert tr[-1]["done"] and not any(r["done"] for r in tr[1:-1])
 
 
 @pytest.mark.parametrize("model", ["linear", "mlp"])
