@@ -175,6 +175,39 @@ def run_case(wl, delta, steps, warmup, torch, weights, *, batch=1, eta=0.0, solv
         return timed_samples(s, x, steps, warmup, torch)
 
 
+def measured_ceilings(torch, gemm_m):
+    """Ceilings measured on this GPU beside the vendor peaks: a plain 1 GiB device copy
+    (HBM), and hipBLASLt bf16 GEMMs run as a library through torch.matmul, at the network's
+    GEMM2 shape for one sweep's misses ([gemm_m x 1024] x [1024 x 1024]) and at 8192^3."""
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+    n = (1 << 30) // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    t = timed(lambda: dst.copy_(src), 10)
+    copy_gbs = 2 * n * 4 / t / 1e9
+    del src, dst
+    out = {"copy_1GiB_GBps": copy_gbs}
+    for name, (m, k, nn) in {"gemm2_shape": (gemm_m, 1024, 1024), "square_8192": (8192, 8192, 8192)}.items():
+        A = torch.randn(m, k, device="cuda", dtype=torch.bfloat16)
+        Bm = torch.randn(k, nn, device="cuda", dtype=torch.bfloat16)
+        t = timed(lambda: torch.matmul(A, Bm), 20)
+        out[f"bf16_{name}_TFLOPs"] = 2.0 * m * k * nn / t / 1e12
+        out[f"bf16_{name}"] = [m, k, nn]
+        del A, Bm
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(wl, delta, budget_s):
     """The oracle (as it stands) on a bounded prefix of the same sample."""
     import numpy as np
@@ -353,8 +386,25 @@ def main():
                      "flops_per_launch": p["nfe"] * fpe / max(p["launches"], 1)},
     }
     line.update(extras)
+    if not args.headline_only:
+        ceil = measured_ceilings(torch, int(round(p["nfe"] / p["sweeps"])) * wl.tokens)
+        line["measured_ceilings"] = ceil
+        line["roofline"]["frac_vs_measured_square_gemm"] = achieved / ceil["bf16_square_8192_TFLOPs"]
+        line["roofline"]["frac_vs_measured_gemm2_shape"] = achieved / ceil["bf16_gemm2_shape_TFLOPs"]
+        for key in ("solver_kernels",):
+            pk = line[key]["k_picard"]
+            if pk["achieved"]:
+                pk["frac_vs_measured_copy"] = pk["achieved"] / ceil["copy_1GiB_GBps"]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, PRIMARY_DELTA, args.cpu_seconds)
+        if not args.headline_only:
+            try:
+                from threadpoolctl import threadpool_limits
+                with threadpool_limits(limits=1):
+                    one = cpu_baseline(wl, PRIMARY_DELTA, args.cpu_seconds)
+                line["cpu_baseline_1thread"] = dict(one, cores=1)
+            except ImportError:
+                pass
     print(json.dumps(line), flush=True)
 
 
