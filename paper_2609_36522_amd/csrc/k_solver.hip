@@ -143,10 +143,12 @@ int picard_blocks(int D) { return (D / 4 + kCols - 1) / kCols; }
 
 // LINEAR computes eps = c_t * x for the misses in place; otherwise the fresh outputs are the
 // fixed-order sum of the network kernel's partial outputs.
-template <int TPT, bool LINEAR>
+// NS: partial outputs per fresh network output (the network kernel's splits of the output
+// units; 1 for the linear network).
+template <int TPT, bool LINEAR, int NS>
 __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     const int n = blockIdx.y;
-    Ctrl* ctrl = d.ctrl + n;
+    const Ctrl* ctrl = d.ctrl + n;
     if (ctrl->done) return;
     const int s = ctrl->s, e = ctrl->e, W = e - s, newest = ctrl->newest;
     const int tid = threadIdx.x;
@@ -163,53 +165,98 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
     const double4 dzero = make_double4(0.0, 0.0, 0.0, 0.0);
 
+    // ---- the states (independent of the miss list) first; meanwhile the block stages the
+    // per-slot miss flags and ranks in LDS, so that the address of every other load is known
+    // after one barrier instead of a chain of dependent global byte loads.
     // xs[k] = current estimate of state s + j0 + k (k <= TPT, j0 + k <= W): the drift input of
     // slot j0 + k and the previous iterate of the state slot j0 + k - 1 updates.
-    float4 xs[TPT + 1], xhn[TPT], anchor = zero;
-    double4 dr[TPT];
+    float4 xs[TPT + 1], e0[TPT], ex[TPT][NS > 1 ? NS - 1 : 1], zt[TPT], xhn[TPT];
+    double cf[TPT][3];
+    float4 anchor = zero;
+    if (colok) anchor = reinterpret_cast<const float4*>(X + min(s, newest) * D)[c4];
 #pragma unroll
     for (int k = 0; k <= TPT; ++k) {
         const int j = j0 + k;
-        const int t = min(s + j, newest);
-        xs[k] = (j <= W && colok) ? reinterpret_cast<const float4*>(X + t * D)[c4] : zero;
+        xs[k] = (j <= W && colok) ? reinterpret_cast<const float4*>(X + min(s + j, newest) * D)[c4] : zero;
     }
+    __shared__ uint8_t sm[PA_MAX_WINDOW + TPT + 1];
+    __shared__ uint8_t sr[PA_MAX_WINDOW + TPT];
+    static_assert(kThreads >= PA_MAX_WINDOW, "one thread per window slot");
+    if (tid < W) {
+        sm[tid] = ctrl->slot_miss[tid];
+        sr[tid] = ctrl->slot_rank[tid];
+    }
+    __syncthreads();
+    // f[k]: slot j0 + k is a miss (k <= TPT; slot j0 + TPT decides where the last updated
+    // state's next cache entry comes from); rk[k]: its place in the miss list.
+    int f[TPT + 1], rk[TPT];
+#pragma unroll
+    for (int k = 0; k <= TPT; ++k) f[k] = (j0 + k < W) ? sm[j0 + k] : 0;
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) rk[k] = (j0 + k < W) ? sr[j0 + k] : 0;
+
+    // ---- every other load of the thread, issued before any store.
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
-        const int j = j0 + k;
-        dr[k] = dzero;
+        const int j = j0 + k, t = s + j;
+        const bool act = j < W && colok;
+        const bool miss = f[k] != 0;
+        e0[k] = zero;
+        zt[k] = zero;
         xhn[k] = zero;
+#pragma unroll
+        for (int h = 0; h < (NS > 1 ? NS - 1 : 1); ++h) ex[k][h] = zero;
+        cf[k][0] = cf[k][1] = cf[k][2] = 0.0;
+        if (act) {
+            // Eq. (6): the cached output of a hit, or the network kernel's partial outputs of
+            // a miss (LINEAR: computed below from the state).
+            const float* ep = d.Ep + ((size_t)n * d.P + rk[k]) * D;
+            if (!(LINEAR && miss)) e0[k] = reinterpret_cast<const float4*>(miss ? ep : Eh + t * D)[c4];
+            if (!LINEAR && miss) {
+#pragma unroll
+                for (int h = 1; h < NS; ++h)
+                    ex[k][h - 1] = reinterpret_cast<const float4*>(ep + (size_t)h * d.N * d.P * D)[c4];
+            }
+            cf[k][0] = d.coef[3 * t];
+            cf[k][1] = d.coef[3 * t + 1];
+            if (noise) {
+                cf[k][2] = d.coef[3 * t + 2];
+                zt[k] = reinterpret_cast<const float4*>(noise + t * D)[c4];
+            }
+        }
+        // Cache entry the updated state s + 1 + j is tested against in the next sweep: the
+        // state itself if slot j + 1 is a miss now (its entry is refreshed below), else Xh.
+        if (j + 1 < W && colok && !f[k + 1]) xhn[k] = reinterpret_cast<const float4*>(Xh + (s + 1 + j) * D)[c4];
+    }
+
+    // ---- Eq. (6)-(7) and the drift at the current latents (fp64), cache writes of misses.
+    double4 dr[TPT];
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {
+        const int j = j0 + k, t = s + j;
+        dr[k] = dzero;
+        if (j + 1 < W && f[k + 1]) xhn[k] = xs[k + 1];
         if (j < W && colok) {
-            const int t = s + j;
             const float4 x = xs[k];
-            float4 eps;
-            if (ctrl->slot_miss[j]) {
+            float4 eps = e0[k];
+            if (f[k]) {
                 if (LINEAR) {
                     const float ct = d.lin_c[t];
                     eps = make_float4(ct * x.x, ct * x.y, ct * x.z, ct * x.w);
                 } else {
                     // Fresh output = fixed-order sum of the network kernel's partials.
-                    const float* ep = d.Ep + ((size_t)n * d.P + ctrl->slot_rank[j]) * D;
-                    eps = reinterpret_cast<const float4*>(ep)[c4];
-                    for (int h = 1; h < d.nsplit; ++h) {
-                        const float4 p = reinterpret_cast<const float4*>(ep + (size_t)h * d.N * d.P * D)[c4];
+#pragma unroll
+                    for (int h = 1; h < NS; ++h) {
+                        const float4 p = ex[k][h - 1];
                         eps = make_float4(eps.x + p.x, eps.y + p.y, eps.z + p.z, eps.w + p.w);
                     }
                 }
-                reinterpret_cast<float4*>(Eh + t * D)[c4] = eps;   // Eq. (7) output
-                reinterpret_cast<float4*>(Xh + t * D)[c4] = x;     // Eq. (7) input
-            } else {
-                eps = reinterpret_cast<const float4*>(Eh + t * D)[c4];  // Eq. (6) hit
             }
-            dr[k] = drift(d.coef[3 * t], x, d.coef[3 * t + 1], eps);
-            if (noise) dr[k] = add_noise(dr[k], d.coef[3 * t + 2], reinterpret_cast<const float4*>(noise + t * D)[c4]);
+            dr[k] = drift(cf[k][0], x, cf[k][1], eps);
+            if (noise) dr[k] = add_noise(dr[k], cf[k][2], zt[k]);
+            e0[k] = eps;
         }
-        // Cache entry the updated state s + 1 + j is tested against in the next sweep.
-        if (j + 1 < W && colok)
-            xhn[k] = ctrl->slot_miss[j + 1] ? xs[k + 1]
-                                            : reinterpret_cast<const float4*>(Xh + (s + 1 + j) * D)[c4];
     }
-    if (colok) anchor = reinterpret_cast<const float4*>(X + min(s, newest) * D)[c4];
-
 #pragma unroll
     for (int k = 1; k < TPT; ++k) dr[k] = d4_add(dr[k], dr[k - 1]);
 
@@ -219,24 +266,31 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     tot[row][col] = dr[TPT - 1];
     __builtin_amdgcn_s_waitcnt(0);          // all loads of X consumed before any store below
     __syncthreads();
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {
+        const int j = j0 + k, t = s + j;
+        if (j < W && colok && f[k]) {
+            reinterpret_cast<float4*>(Eh + t * D)[c4] = e0[k];   // Eq. (7) output
+            reinterpret_cast<float4*>(Xh + t * D)[c4] = xs[k];   // Eq. (7) input
+        }
+    }
     double4 pre = d4_of(anchor);
     for (int r = 0; r < row; ++r) pre = d4_add(pre, tot[r][col]);
 
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
         const int j = j0 + k;
-        if (j >= W) break;                  // uniform over the 16-lane row
-        const double4 yd = d4_add(pre, dr[k]);
-        const float4 y = make_float4((float)yd.x, (float)yd.y, (float)yd.z, (float)yd.w);
         double rs = 0.0, ds = 0.0;
-        if (colok) {
+        if (j < W && colok) {
+            const double4 yd = d4_add(pre, dr[k]);
+            const float4 y = make_float4((float)yd.x, (float)yd.y, (float)yd.z, (float)yd.w);
             reinterpret_cast<float4*>(X + (s + 1 + j) * D)[c4] = y;
             rs = sq_dev(y, xs[k + 1]);                   // Eq. (2) vs the previous iterate
             if (j + 1 < W) ds = abs_dev(y, xhn[k]);      // Eq. (4) for the next sweep
         }
-        rs = group_sum<kCols>(rs);
+        rs = group_sum<kCols>(rs);                       // j is uniform over the 16-lane row
         ds = group_sum<kCols>(ds);
-        if (col == 0) {
+        if (col == 0 && j < W) {
             rres[j] = rs;
             rdev[j] = ds;
         }
@@ -251,22 +305,28 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     }
 }
 
-template <bool LINEAR>
+template <bool LINEAR, int NS>
 static hipError_t launch_picard_t(const Dev& d, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const dim3 grid(d.picard_blocks, d.N), block(kThreads);
     switch (picard_tpt(d.P)) {
-        case 1: hipExtLaunchKernelGGL((k_picard<1, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 2: hipExtLaunchKernelGGL((k_picard<2, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 4: hipExtLaunchKernelGGL((k_picard<4, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 8: hipExtLaunchKernelGGL((k_picard<8, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 16: hipExtLaunchKernelGGL((k_picard<16, LINEAR>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 1: hipExtLaunchKernelGGL((k_picard<1, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 2: hipExtLaunchKernelGGL((k_picard<2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 4: hipExtLaunchKernelGGL((k_picard<4, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 8: hipExtLaunchKernelGGL((k_picard<8, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 16: hipExtLaunchKernelGGL((k_picard<16, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t e0, hipEvent_t e1) {
-    return linear ? launch_picard_t<true>(d, st, e0, e1) : launch_picard_t<false>(d, st, e0, e1);
+    if (linear) return launch_picard_t<true, 1>(d, st, e0, e1);
+    switch (d.nsplit) {
+        case 1: return launch_picard_t<false, 1>(d, st, e0, e1);
+        case 2: return launch_picard_t<false, 2>(d, st, e0, e1);
+        case 4: return launch_picard_t<false, 4>(d, st, e0, e1);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 // ---------------------------------------------------------------------------- slide
