@@ -75,7 +75,9 @@ def parse():
     ap.add_argument("--deltas", type=str, default="0,0.02,0.05,0.1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--headline-only", action="store_true",
-                    help="skip the revisit, batched and DDPM measurements")
+                    help="skip the revisit, batched, DDPM and Parareal measurements")
+    ap.add_argument("--extras", type=str, default="revisit,batched,ddpm,parareal",
+                    help="which extra measurements to run (comma list)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle's bounded sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -262,8 +264,9 @@ def main():
 
     extras = {}
     if not args.headline_only:
+        want = set(args.extras.split(","))
         # revisit statistic of the delta = 0 run (the cache's motivation figure, Sec. 1)
-        if 0.0 in per_delta:
+        if "revisit" in want and 0.0 in per_delta:
             r0 = per_delta[0.0]
             req = r0["nfe"] + r0["hits"]
             extras["revisit_statistic"] = {
@@ -271,6 +274,7 @@ def main():
                 "fraction_of_requests": r0["revisits_below"] / req,
                 "revisit_fraction": r0["revisits"] / req,
                 "requests_per_sample": req / args.steps}
+    if not args.headline_only and "batched" in want:
         # several samples per handle
         nb = 8
         bsteps = max(args.steps // 3, 3)
@@ -287,6 +291,7 @@ def main():
                 run_case(wl, PRIMARY_DELTA, 3, 1, torch, weights, batch=nb, solver=True), wl.D)}
         print(f"[bench] batch {nb}: {extras['batched']['ms_per_batch']:.3f} ms/batch, "
               f"{extras['batched']['samples_per_s']:.0f} samples/s", file=sys.stderr, flush=True)
+    if not args.headline_only and "ddpm" in want:
         # the window study's stochastic setting
         wd = wl.with_(T=1000, window=64)
         dsteps = max(args.steps // 6, 3)
@@ -305,6 +310,7 @@ def main():
                                    "sweeps_per_sample": r["sweeps"] / dsteps}
                           for d, r in dd.items()},
             "nfe_saved_vs_delta0": 1.0 - dd[PRIMARY_DELTA]["nfe"] / dd[0.0]["nfe"]}
+    if not args.headline_only and "parareal" in want:
         # the Parareal-style cached sampler
         wp = workloads.PARAREAL_MLP
         wts = inputs.mlp_weights(wp.hidden, temb_dim=wp.temb_dim)
