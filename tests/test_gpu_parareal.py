@@ -41,6 +41,7 @@ CASES = [
     ("lin_one_block", _wl("pr_lin_4x8x8_T10_B1", (4, 8, 8), 10, 1), 0.05),
     ("lin_unit_blocks", _wl("pr_lin_4x8x8_T8_B8", (4, 8, 8), 8, 8), 0.05),
     ("lin_c5_shape", _wl("pr_lin_4x96x96_T100_B10", (4, 96, 96), 100, 10), 0.05),
+    ("lin_max_blocks", _wl("pr_lin_4x8x8_T64_B64", (4, 8, 8), 64, 64), 0.05),
     ("mlp_small", _wl("pr_mlp_4x32x32_T20_B4_H512", (4, 32, 32), 20, 4, "patch_mlp", 512), 0.05),
     ("mlp_c5", W.PARAREAL_MLP, 0.05),
     ("mlp_c5_delta0", W.PARAREAL_MLP, 0.0),

@@ -57,6 +57,12 @@ CASES = [
     ("ddpm_batch3_tiny", LIN, 0.05, dict(eta=1.0, batch=3)),
     ("ddpm_mlp_small", W.SMALL_MLP, 0.05, dict(eta=1.0)),
     ("ddpm_eta_half", W.SMALL_MLP, 0.05, dict(eta=0.5)),
+    # widest network (four partial outputs per fresh output) in the Picard sampler
+    ("mlp_H2048", Workload("mlp_4x32x32_T20_P8_H2048", (4, 32, 32), 20, 8, 0.05, 1e-3, "patch_mlp",
+                           hidden=2048), 0.05),
+    # largest batch: the network kernel's prefix over 64 samples
+    ("batch64_mlp", Workload("mlp_4x16x32_T12_P6_H512", (4, 16, 32), 12, 6, 0.05, 1e-3, "patch_mlp",
+                             hidden=512), 0.05, dict(batch=64)),
 ]
 CASES = [c if len(c) == 4 else (*c, {}) for c in CASES]
 
