@@ -240,7 +240,7 @@ def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the sampler has no "
-              f"multi-GPU path in this build.", file=sys.stderr, flush=True)
+              f"multi-GPU path.", file=sys.stderr, flush=True)
         sys.exit(2)
     import torch
     from paper_2609_36522_amd import binding, inputs, workloads

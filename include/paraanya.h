@@ -50,7 +50,7 @@ extern "C" {
 #define PA_ERR_OOM         (-3)  /* device or pinned-host allocation failed */
 #define PA_ERR_STATE       (-4)  /* call not valid in the handle's current state */
 #define PA_ERR_NONFINITE   (-5)  /* a residual of Eq. (2) was NaN/Inf; the sweep completed */
-#define PA_ERR_UNSUPPORTED (-6)  /* valid request this build does not implement */
+#define PA_ERR_UNSUPPORTED (-6)  /* valid request the library does not implement */
 
 #define PA_MAX_WINDOW 256        /* largest window P */
 #define PA_MAX_BATCH  64         /* largest number of samples N per handle */

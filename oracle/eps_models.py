@@ -1,7 +1,7 @@
 """Synthetic noise-prediction networks eps(x, j) (oracle; test infrastructure only).
 
 The paper evaluates the Stable Diffusion v1.5 UNet (Sec. 3.2); its weights are not
-available, so two synthetic networks stand in for it (readings R15, R16 in the design doc):
+available, so two synthetic networks stand in for it (readings where the paper is silent):
 
 * linear:    eps_j(x) = c_j * x, one fp32 multiply per element (exact in fp64, then
              rounded once to the storage type);

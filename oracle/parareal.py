@@ -3,11 +3,11 @@
 Sec. 2.1 describes Parareal-based samplers (SRDS) as a coarse solver that initializes the
 trajectory and fine solvers that refine it; Sec. 2.2 applies the same cache to their
 network evaluations, leaving the Parareal update rule unchanged. The paper does not print
-the update rule; the textbook Parareal iteration is used (reading R24):
+the update rule; the textbook Parareal iteration is used (a reading):
 
 * T sampling steps split into B blocks of L = T / B fine steps; boundary n is state nL.
 * Fine propagator F_n(u): L serial DDIM steps from state nL, x_{t+1} = x_t + d_t with the
-  drift d_t = alpha_t x_t + b_t eps(x_t, t) of the fine grid (R1).
+  drift d_t = alpha_t x_t + b_t eps(x_t, t) of the fine grid (the DDIM one-step increment).
 * Coarse propagator G_n(u): one DDIM step from state nL to state (n+1)L,
   u + (ac_n u + bc_n eps(u, nL)), with ac_n = sqrt(ab_{(n+1)L} / ab_{nL}) - 1 and
   bc_n = sqrt(1 - ab_{(n+1)L}) - (1 + ac_n) sqrt(1 - ab_{nL}).

@@ -6,7 +6,7 @@ deviation, first-entry miss rule, Eq. (5) hit/miss partition, Eq. (6) assembly, 
 batched evaluation of the misses, Eq. (7) miss-only cache update, and the drift taken
 at the current latent with the assembled network output).
 
-Readings where the paper is silent (the design doc lists them as R1-R20):
+Readings where the paper is silent:
 
 * the drift of Eq. (1) is the DDIM one-step increment d_i = alpha_i x_i + b_i eps_i;
 * the Picard sum is anchored at the window start s (whose state is final);
@@ -16,7 +16,7 @@ Readings where the paper is silent (the design doc lists them as R1-R20):
 * states that enter the window start as copies of the newest computed state;
 * misses are listed in ascending t; hit test is strict '<' (Eq. (5)).
 
-Stochastic steps (reading R21): with pre-drawn step noise z_i and scale sigma_i the drift
+Stochastic steps (a reading; the paper names DDPM but prints no step): with pre-drawn step noise z_i and scale sigma_i the drift
 gains the term sigma_i z_i, which is the same in every sweep; ``noise`` below is the array
 of those terms, [T, D] (None for the deterministic sampler).
 

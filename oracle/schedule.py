@@ -3,7 +3,7 @@
 The paper samples Stable Diffusion v1.5 with DDIM (Sec. 3.3) and writes the drift
 s_theta of Eq. (1) as a combination of the current latent and the noise prediction
 with schedule-determined coefficients (Sec. 2.1). It does not print the schedule;
-the reading used here (readings R1 and R14):
+the reading used here:
 
 * training betas "scaled linear": beta_j = (sqrt(b0) + j (sqrt(b1) - sqrt(b0)) / (N-1))^2,
   j = 0..N-1, with b0 = 0.00085, b1 = 0.012, N = 1000; alpha_bar_j = prod_{i<=j} (1 - beta_i);
@@ -17,8 +17,7 @@ the reading used here (readings R1 and R14):
 * the stochastic sampler of the window study (DDPM, Sec. 3.4) is the generalized DDIM step
   with eta = 1: x_{i+1} = sqrt(ab_{i+1}) x0^ + sqrt(1 - ab_{i+1} - sigma_i^2) eps + sigma_i z_i,
   sigma_i = eta sqrt((1 - ab_{i+1}) / (1 - ab_i)) sqrt(1 - ab_i / ab_{i+1}), with the noise
-  z_i drawn before sampling so that the Picard iteration solves a fixed recurrence
-  (reading R21).
+  z_i drawn before sampling so that the Picard iteration solves a fixed recurrence.
 
 Everything is float64.
 """

@@ -24,7 +24,7 @@ from oracle import sampler as sp
 from oracle import schedule as sch
 from paper_2609_36522_amd import binding, inputs
 
-# Tolerances, derived from the arithmetic ("Parity tolerances"):
+# Tolerances, derived from the arithmetic:
 # both sides form the drift, the Picard sum, the deviations and the residuals in fp64 from
 # the same fp32 inputs; they differ only in the association of fp64 sums (~1e-16 relative),
 # so an updated fp32 state can differ by at most one fp32 ulp (a rounding tie), and a

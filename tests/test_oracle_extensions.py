@@ -1,7 +1,7 @@
 """Pins for the oracle's extensions beyond the deterministic single-sample sampler. CPU only.
 
 Stochastic step (ancestral DDPM with pre-drawn step noise, the window study's sampler,
-Sec. 3.4; reading R21):
+Sec. 3.4; the generalized DDIM step with eta = 1, the paper printing no step):
   * eta = 0 gives the DDIM coefficients; the last step (alpha_bar = 1) carries no noise;
   * window = 1 reproduces serial DDPM in its textbook (posterior mean + variance) form,
     which is written without the generalized-DDIM coefficients;

@@ -1,5 +1,5 @@
 """Pins for the oracle's cached Parareal sampler (Sec. 2.1 Parareal-based samplers, Sec. 2.2
-cache; reading R24). CPU only.
+cache; the textbook Parareal predictor-corrector, the paper printing no rule). CPU only.
 
 * delta = 0 reproduces the uncached Parareal iteration exactly.
 * Parareal exactness: after k iterations the boundaries 0..k equal serial fine DDIM bit for
