@@ -90,26 +90,22 @@ def timed_samples(sampler, x, steps, warmup, torch):
     for _ in range(warmup):                         # untimed warm-up generations
         sampler.sample(x, out)
     torch.cuda.synchronize()
+    sampler.kernel_times()                          # restart the kernel timers
     sweeps = nfe = hits = revisits = below = 0
-    eps_ms = picard_ms = slide_ms = 0.0
-    launches = solver_launches = 0
     t0 = time.perf_counter()
     for _ in range(steps):
         sampler.sample(x, out)
-        st = sampler.stats()
-        kt = sampler.kernel_times()
+        st = sampler.stats()                        # host mirror of the last synchronization
         sweeps += st["sweeps"]
         nfe += st["nfe"]
         hits += st["hits"]
         revisits += st["revisits"]
         below += st["revisits_below"]
-        eps_ms += kt["eps_ms_total"]
-        launches += kt["launches"]
-        picard_ms += kt["picard_ms_total"]
-        slide_ms += kt["slide_ms_total"]
-        solver_launches += kt["solver_launches"]
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    kt = sampler.kernel_times()                     # every launch of the timed samples
+    eps_ms, launches = kt["eps_ms_total"], kt["launches"]
+    picard_ms, slide_ms, solver_launches = kt["picard_ms_total"], kt["slide_ms_total"], kt["solver_launches"]
     return {"seconds": dt, "sweeps": sweeps, "nfe": nfe, "hits": hits, "eps_ms": eps_ms,
             "launches": launches, "revisits": revisits, "revisits_below": below,
             "picard_ms": picard_ms, "slide_ms": slide_ms, "solver_launches": solver_launches,
@@ -125,20 +121,19 @@ def parareal_case(wl, delta, steps, warmup, torch, weights):
         for _ in range(warmup):
             s.sample(x, out)
         torch.cuda.synchronize()
-        nfe = hits = iters = launches = 0
-        eps_ms = 0.0
+        s.kernel_times()                            # restart the kernel timers
+        nfe = hits = iters = 0
         t0 = time.perf_counter()
         for _ in range(steps):
             s.sample(x, out)
             st = s.stats()
-            kt = s.kernel_times()
             nfe += st["nfe"]
             hits += st["hits"]
             iters += st["iterations"]
-            eps_ms += kt["eps_ms_total"]
-            launches += kt["launches"]
         torch.cuda.synchronize()
         dt = time.perf_counter() - t0
+        kt = s.kernel_times()
+        eps_ms, launches = kt["eps_ms_total"], kt["launches"]
     return {"seconds": dt, "nfe": nfe, "hits": hits, "iters": iters, "eps_ms": eps_ms,
             "launches": launches}
 

@@ -236,7 +236,10 @@ PA_API int paraanya_read_state_sample(paraanya_t* h, int32_t n, int32_t t0, int3
  * fp32 time-embedding table e[T][hidden]. */
 PA_API int paraanya_coefficients(paraanya_t* h, double* alpha, double* b, double* sigma, float* temb);
 
-/* Kernel timings since reset (PA_FLAG_PROFILE); synchronizes. STATE without it. */
+/* Kernel timings (PA_FLAG_PROFILE) of every launch since the previous call (or since
+ * create): the totals restart after each call, so a caller can time many samples and read
+ * once. eps_latents counts the network latents of the completed samples among them.
+ * Synchronizes. STATE without the flag. */
 PA_API int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out);
 
 /* Free every resource of the handle (synchronizes its stream first). NULL-safe. */
@@ -309,7 +312,8 @@ PA_API int paraanya_parareal_residuals(paraanya_parareal_t* h, int32_t k, double
 /* Test hook: the boundary states U_0..U_B of the last sample, host (B+1) x D fp32. */
 PA_API int paraanya_parareal_read_boundaries(paraanya_parareal_t* h, float* U);
 
-/* Network-launch timings of the last sample (PA_FLAG_PROFILE); STATE without it. */
+/* Network-launch timings since the previous call (or create), as paraanya_kernel_times;
+ * STATE without PA_FLAG_PROFILE. */
 PA_API int paraanya_parareal_kernel_times(paraanya_parareal_t* h, pa_ktimes_t* out);
 
 /* Free the handle (synchronizes its stream first). NULL-safe. */

@@ -31,6 +31,7 @@ struct paraanya {
     bool host_done = false;           // done flag of the last synchronized read
     pa::DevMem mem;                   // device allocations
     pa::KernelTimer timer;            // kinds: 0 network, 1 Picard, 2 slide
+    int64_t timed_latents = 0;        // network latents of the samples the timer covers
 
     ~paraanya() {
         (void)hipStreamSynchronize(stream);
@@ -205,7 +206,6 @@ int paraanya_reset(paraanya_t* h, const float* x_init) {
     PA_HIP(pa::launch_reset(h->d, h->stream));
     h->have_reset = true;
     h->host_done = false;
-    h->timer.clear();
     return PA_OK;
 }
 
@@ -301,6 +301,7 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
                             (size_t)N, hipMemcpyDeviceToDevice, h->stream));
     h->ctrl_fresh = false;
     if ((rc = h->read_ctrl())) return rc;
+    for (int n = 0; n < N; ++n) h->timed_latents += h->ctrl_host[n].nfe;
     if (h->any_nonfinite()) return fail(PA_ERR_NONFINITE, "non-finite residual during sampling");
     return PA_OK;
 }
@@ -433,8 +434,9 @@ int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out) {
     out->solver_launches = h->timer.launches[1];
     out->picard_ms_total = h->timer.ms[1];
     out->slide_ms_total = h->timer.ms[2];
-    out->eps_latents = 0;
-    for (int n = 0; n < h->d.N; ++n) out->eps_latents += h->ctrl_host[n].nfe;
+    out->eps_latents = h->timed_latents;
+    h->timer.clear();
+    h->timed_latents = 0;
     return PA_OK;
 }
 

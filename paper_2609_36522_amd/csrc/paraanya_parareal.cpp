@@ -34,6 +34,8 @@ struct paraanya_parareal {
     uint64_t* progress_host = nullptr;
     pa::DevMem mem;
     pa::KernelTimer timer;
+    int64_t timed_latents = 0;        // network latents of the samples the timer covers
+    pa_parareal_stats_t last{};       // counters of the last sample, read at its end
 
     ~paraanya_parareal() {
         (void)hipStreamSynchronize(stream);
@@ -189,7 +191,6 @@ int paraanya_parareal_sample(paraanya_parareal_t* h, const float* x_init, float*
     const size_t D = (size_t)d.D, rows = (size_t)T + 1;
     PA_HIP(hipStreamSynchronize(h->stream));      // nothing of an earlier sample still runs
     *h->progress_host = 0;
-    h->timer.clear();
     PA_HIP(hipMemcpyAsync(d.X, x_init, D * sizeof(float), hipMemcpyDeviceToDevice, h->stream));
     PA_HIP(pa::launch_pr(d, h->args(pa::PR_INIT, 0, 0, 0, 0), pa::PRK_RESET, h->stream));
     int rc, rec = 0;
@@ -214,8 +215,21 @@ int paraanya_parareal_sample(paraanya_parareal_t* h, const float* x_init, float*
     PA_HIP(hipMemcpyAsync(x_out, d.X + ((size_t)B * rows + T) * D, D * sizeof(float),
                           hipMemcpyDeviceToDevice, h->stream));
     PrCtrl pc;
+    std::vector<Ctrl> c((size_t)B);
     PA_HIP(hipMemcpyAsync(&pc, h->pc, sizeof(PrCtrl), hipMemcpyDeviceToHost, h->stream));
+    PA_HIP(hipMemcpyAsync(c.data(), d.ctrl, c.size() * sizeof(Ctrl), hipMemcpyDeviceToHost, h->stream));
     PA_HIP(hipStreamSynchronize(h->stream));
+    pa_parareal_stats_t& st = h->last;
+    memset(&st, 0, sizeof st);
+    for (const Ctrl& x : c) {
+        st.nfe += x.nfe;
+        st.hits += x.hits;
+    }
+    st.requests = st.nfe + st.hits;
+    st.iterations = pc.iters;
+    st.done = pc.done;
+    st.nonfinite = pc.nonfinite;
+    h->timed_latents += st.nfe;
     if (pc.nonfinite) return fail(PA_ERR_NONFINITE, "non-finite boundary residual");
     return PA_OK;
 }
@@ -224,20 +238,7 @@ int paraanya_parareal_stats(paraanya_parareal_t* h, pa_parareal_stats_t* out) {
     pa::g_err.clear();
     if (!h || !out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
     if (!h->have_sample) return fail(PA_ERR_STATE, "stats before the first sample");
-    std::vector<Ctrl> c((size_t)h->B);
-    PrCtrl pc;
-    PA_HIP(hipStreamSynchronize(h->stream));
-    PA_HIP(hipMemcpy(c.data(), h->d.ctrl, c.size() * sizeof(Ctrl), hipMemcpyDeviceToHost));
-    PA_HIP(hipMemcpy(&pc, h->pc, sizeof(PrCtrl), hipMemcpyDeviceToHost));
-    memset(out, 0, sizeof *out);
-    for (const Ctrl& x : c) {
-        out->nfe += x.nfe;
-        out->hits += x.hits;
-    }
-    out->requests = out->nfe + out->hits;
-    out->iterations = pc.iters;
-    out->done = pc.done;
-    out->nonfinite = pc.nonfinite;
+    *out = h->last;   // read back at the end of the sample; nothing has run since
     return PA_OK;
 }
 
@@ -288,12 +289,12 @@ int paraanya_parareal_kernel_times(paraanya_parareal_t* h, pa_ktimes_t* out) {
     PA_HIP(hipStreamSynchronize(h->stream));
     int rc = h->timer.drain();
     if (rc) return rc;
-    pa_parareal_stats_t st;
-    if ((rc = paraanya_parareal_stats(h, &st))) return rc;
     memset(out, 0, sizeof *out);
     out->launches = h->timer.launches[0];
     out->eps_ms_total = h->timer.ms[0];
-    out->eps_latents = st.nfe;
+    out->eps_latents = h->timed_latents;
+    h->timer.clear();
+    h->timed_latents = 0;
     return PA_OK;
 }
 
