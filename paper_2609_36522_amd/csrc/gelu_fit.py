@@ -3,14 +3,21 @@
     python paper_2609_36522_amd/csrc/gelu_fit.py
 
 GELU(x) = x Phi(x) = max(x, 0) - a Q(a),  a = |x|,  Q(a) = 1 - Phi(a) the normal upper tail.
-The kernel evaluates Q(a) = 2^(-P(min(a, A_MAX))) with P a polynomial in a, i.e. one v_exp_f32
-and a Horner chain of fused multiply-adds. P is fitted to -log2(Q(a)) on [0, A_MAX] by
-iteratively reweighted least squares toward the minimax (equal-ripple) solution of the
-absolute error of P, which is the relative error of Q (times ln 2). Above A_MAX,
-a Q(a) < 2.2e-7 a, so clamping the argument costs at most that much.
+The kernels evaluate twice the GELU,
 
-Prints the coefficients (low to high degree, as float32 literals) and the accuracy of the
-float32 evaluation against scipy's erf in float64.
+    2 GELU(x) = (x + a) - a 2Q(a),   2Q(a) = 2^(-(P(a) - 1)),
+
+with P a polynomial in a: one v_add_f32 (x + a = 2 max(x, 0) exactly), a Horner chain of
+fused multiply-adds whose constant term is lowered by 1, one v_exp_f32 and one last FMA. The
+factor 2 is exact and is undone in the next product (the following weight matrix is stored
+halved). P is fitted to -log2(Q(a)) on [0, A_MAX] by iteratively reweighted least squares
+toward the minimax (equal-ripple) solution of the absolute error of P, which is the relative
+error of Q (times ln 2). The argument is not clamped: the script checks that P increases
+monotonically well beyond A_MAX and keeps tracking -log2 Q there, so that a Q(a) stays tiny
+(and P overflows to +inf, Q to 0, for huge a).
+
+Prints the coefficients (low to high degree, as float32 literals), the constant term used by
+the kernels, and the accuracy of the float32 evaluation against scipy's erf in float64.
 """
 from __future__ import annotations
 
@@ -36,26 +43,37 @@ def fit(deg=DEG, amax=A_MAX, iters=60):
     return poly.astype(np.float32)
 
 
-def gelu_f32(x, coef, amax=A_MAX):
+def gelu2_f32(x, coef):
+    """Float32 emulation of the kernels' 2 GELU(x) (v_exp_f32 taken as correctly rounded)."""
     f32 = np.float32
     x = x.astype(f32)
-    a = np.minimum(np.abs(x), f32(amax))
-    p = np.full_like(a, coef[-1])
-    for k in range(len(coef) - 2, -1, -1):
-        p = (p * a + coef[k]).astype(f32)
-    q = np.exp2(-p.astype(np.float64)).astype(f32)          # v_exp_f32 ~ correctly rounded
-    return (np.maximum(x, f32(0)) - np.abs(x) * q).astype(f32)
+    a = np.abs(x)
+    c = coef.copy()
+    c[0] = f32(c[0] - f32(1))                                  # P(a) - 1
+    p = np.full_like(a, c[-1])
+    for k in range(len(c) - 2, -1, -1):
+        p = (p * a + c[k]).astype(f32)
+    with np.errstate(over="ignore"):
+        q2 = np.exp2(-p.astype(np.float64)).astype(f32)
+    return ((x + a) - a * q2).astype(f32)
 
 
 def report(coef):
     x = np.linspace(-12, 12, 2_400_001)
-    ref = 0.5 * x * (1 + erf(x / np.sqrt(2)))
-    g = gelu_f32(x, coef).astype(np.float64)
+    ref = x * (1 + erf(x / np.sqrt(2)))                        # twice the GELU
+    g = gelu2_f32(x, coef).astype(np.float64)
     e = np.abs(g - ref)
     rel = e / np.maximum(np.abs(ref), 1e-300)
     print(f"max |err| / max(1,|x|)      = {np.max(e / np.maximum(np.abs(x), 1)):.3e}")
     print(f"max rel err, x > 0.01       = {rel[x > 0.01].max():.3e}")
     print(f"max rel err, -4 < x < -0.01 = {rel[(x < -0.01) & (x > -4)].max():.3e}")
+    a = np.linspace(0, 200, 2_000_001)
+    P = np.polynomial.Polynomial(coef.astype(np.float64))(a)
+    print(f"P increasing on [0, 200]    = {bool(np.all(np.diff(P) > 0))}")
+    t = np.array([5.0, 6.0, 8.0, 10.0])
+    qa = np.exp2(-np.polynomial.Polynomial(coef.astype(np.float64))(t))
+    qt = 0.5 * erfc(t / np.sqrt(2.0))
+    print("Q(a) fitted / exact above A_MAX: " + ", ".join(f"a={u:g}: {v:.4f}" for u, v in zip(t, qa / qt)))
 
 
 if __name__ == "__main__":
@@ -63,4 +81,5 @@ if __name__ == "__main__":
     print("coefficients (low -> high):")
     for k, v in enumerate(c):
         print(f"  c{k} = {float(v)!r}f")
+    print(f"constant term used by the kernels (c0 - 1): {float(np.float32(c[0] - np.float32(1)))!r}f")
     report(c)

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <string.h>
 
 #include <hip/hip_ext.h>
 
@@ -137,6 +138,20 @@ void KernelTimer::clear() {
     }
 }
 
+// Half of a bf16 value (bit pattern in, bit pattern out), rounded to nearest even. Exact for
+// every normal value (the exponent drops by one); only a subnormal with its lowest mantissa bit
+// set, or the smallest normal's odd neighbours, round.
+static uint16_t bf16_half(uint16_t b) {
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    f *= 0.5f;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)(u >> 16);   // inf / NaN
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
 int setup_network(Dev& d, DevMem& mem, const pa_eps_model_t* em, const std::vector<double>& tv,
                   int cus, size_t ep_rows, hipStream_t st) {
     const int T = d.T;
@@ -154,7 +169,8 @@ int setup_network(Dev& d, DevMem& mem, const pa_eps_model_t* em, const std::vect
     d.mlp_grid = mlp_grid_size(cus);
     // Device layouts: W1^T [H][16]; W2^T as MFMA A fragments, fragment (b, ks) = lanes
     // l = 0..63 x 8 values W2[16 ks + 8 (l/32) + i][32 b + l%32]; W3 fragments permuted
-    // to the GEMM2 accumulator layout (see k_epsnet.hip).
+    // to the GEMM2 accumulator layout (see k_epsnet.hip). W2 and W3 are stored halved: the
+    // kernels feed them twice the GELU outputs, so every product is the unscaled one.
     std::vector<uint16_t> w1t((size_t)Hd * 16), w2f((size_t)Hd * Hd), w3p((size_t)Hd * 32);
     for (int f = 0; f < 16; ++f)
         for (int n = 0; n < Hd; ++n) w1t[(size_t)n * 16 + f] = em->w1[(size_t)f * Hd + n];
@@ -164,7 +180,7 @@ int setup_network(Dev& d, DevMem& mem, const pa_eps_model_t* em, const std::vect
             for (int lane = 0; lane < 64; ++lane)
                 for (int i = 0; i < 8; ++i) {
                     const int n = b * 32 + (lane & 31), k = ks * 16 + (lane >> 5) * 8 + i;
-                    w2f[(((size_t)b * KS + ks) * 64 + lane) * 8 + i] = em->w2[(size_t)k * Hd + n];
+                    w2f[(((size_t)b * KS + ks) * 64 + lane) * 8 + i] = bf16_half(em->w2[(size_t)k * Hd + n]);
                 }
     for (int hbg = 0; hbg < Hd / 32; ++hbg)
         for (int jj = 0; jj < 2; ++jj)
@@ -173,7 +189,7 @@ int setup_network(Dev& d, DevMem& mem, const pa_eps_model_t* em, const std::vect
                     const int g = lane >> 5, f = lane & 31;
                     const int n = hbg * 32 + (jj * 2 + i / 4) * 8 + g * 4 + (i % 4);
                     w3p[(((size_t)hbg * 2 + jj) * 64 + lane) * 8 + i] =
-                        f < 16 ? em->w3[(size_t)n * 16 + f] : (uint16_t)0;
+                        f < 16 ? bf16_half(em->w3[(size_t)n * 16 + f]) : (uint16_t)0;
                 }
     __bf16 *w1d, *w2d, *w3d, *wtd;
     double* tvd;

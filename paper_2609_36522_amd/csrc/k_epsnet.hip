@@ -6,8 +6,9 @@
 // its ascending order); a prefix over the samples' miss counts maps a list entry back to
 // (sample, miss). For one item the block
 //   0. gathers the 128 tokens (2x2 patches, 16 features) of latent x_t, rounds to bf16;
-//   1. h1^T = GELU(W1^T x^T + e_t) in K-chunks of 256 units: MFMA 32x32x16 bf16, K = 16; bf16
-//      result in LDS ([token][unit], padded rows), two chunk buffers of 66 KB;
+//   1. h1^T = GELU(W1^T x^T + e_t) in K-chunks of 256 units: MFMA 32x32x16 bf16, K = 16, e_t as
+//      the accumulator's initial value; bf16 result (as 2 h1, with W2 stored halved) in LDS
+//      ([token][unit], padded rows), two chunk buffers of 66 KB;
 //   2. h2^T += W2^T h1^T chunk by chunk: each of the 8 waves owns 64 output units x 128
 //      tokens (128 accumulator registers); W2^T fragments stream from L2 in MFMA-fragment
 //      order (1 KB contiguous per wave load), two register stages in flight; the GEMM1 and
@@ -47,26 +48,31 @@ constexpr int kKC = 256;                // h1 units per LDS buffer (K-chunk); tw
 constexpr int kWaves = 8;               // wave w owns output units [64w, 64w + 64) of the item
 constexpr int kFeat = 16;               // 2x2 patch x 4 channels
 constexpr int kXRow = kFeat + 8;        // padded LDS row of the token tile (bf16)
-constexpr int kInterleave = 0;          // VALU instructions scheduled after each GEMM2 MFMA (0: free)
 
-// erf-GELU, x * Phi(x) = max(x, 0) - a Q(a) with a = |x| and Q the normal upper tail,
-// branch-free. Q(a) = 2^(-P(min(a, 5))) with P a degree-7 polynomial fitted toward the
-// minimax relative error of Q (derivation: gelu_fit.py). One v_exp_f32 and eight FMA-class
-// instructions per element; in fp32 the result is within 5.1e-7 max(1, |x|) of the exact
-// erf GELU and within 2.3e-6 (x > 0) / 4.1e-6 (x < 0) relative. Every GELU output is
+// Twice the erf-GELU: 2 x Phi(x) = (x + a) - a 2Q(a) with a = |x| and Q the normal upper tail,
+// branch-free (x + a = 2 max(x, 0) exactly). 2Q(a) = 2^(-(P(a) - 1)) with P a degree-7
+// polynomial fitted toward the minimax relative error of Q on [0, 5] (derivation:
+// gelu_fit.py), its constant term lowered by 1. P increases monotonically for all a >= 0 and
+// keeps tracking -log2 Q above 5 (relative error of Q below 5% up to a = 10, where
+// a Q(a) < 1e-22); for very large a it overflows to +inf and Q to 0, so no clamp is needed.
+// One v_add_f32, eight FMAs and one v_exp_f32 per element; in fp32 the result is within
+// 1.0e-6 max(1, |x|) of twice the exact erf GELU and within 2.3e-6 (x > 0) / 4.1e-6 (x < 0)
+// relative. The factor 2 is exact and is undone exactly in the next product: W2 and W3 are
+// stored halved (bf16 halving is exact for normal values), and bf16(2g) = 2 bf16(g), so every
+// bf16 x bf16 product equals the one with GELU(x) and the unhalved weight. Every GELU output is
 // rounded to bf16 next; the residual error is kept near the fp32 accumulation error of the
 // products so that it adds few rounding flips of its own.
-__device__ __forceinline__ float gelu_erf(float x) {
-    const float a = fminf(fabsf(x), 5.0f);
+__device__ __forceinline__ float gelu2_erf(float x) {
+    const float a = fabsf(x);
     float p = fmaf(a, 1.601676331119961e-06f, -5.784422319266014e-05f);
     p = fmaf(p, a, 0.0009071276872418821f);
     p = fmaf(p, a, -0.008436893112957478f);
     p = fmaf(p, a, 0.05385196581482887f);
     p = fmaf(p, a, 0.45854055881500244f);
     p = fmaf(p, a, 1.1512316465377808f);
-    p = fmaf(p, a, 0.9999960660934448f);
-    const float q = __builtin_amdgcn_exp2f(-p);
-    return fmaf(-fabsf(x), q, fmaxf(x, 0.0f));
+    p = fmaf(p, a, -3.933906555175781e-06f);   // P(a) - 1
+    const float q2 = __builtin_amdgcn_exp2f(-p);  // 2 Q(a)
+    return fmaf(-a, q2, x + a);
 }
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -135,28 +141,27 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     const f32x16 zero16 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
                            0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     const bf16x8* w2lane = reinterpret_cast<const bf16x8*>(d.w2f) + lane;
-
-    for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        const int ns = item % NS;
-        const int rest = item / NS;
-        const int tb = rest % nblk, gm = rest / nblk;
+    // One half (output units [512 ns, 512 ns + 512)) of the item (list entry gm, token block tb).
+    auto half = [&](int gm, int tb, int ns) {
         int n = 0;
         while (mpre[n + 1] <= gm) ++n;               // sample of list entry gm (uniform)
         const int jm = gm - mpre[n];
         const Ctrl* ctrl = d.ctrl + n;
         const int t = ctrl->miss_idx[jm];
-        const float* xt = d.X + ((size_t)n * (d.T + 1) + min(t, ctrl->newest)) * d.D;   // beyond newest: its copy
-        const float* et = d.temb + (size_t)t * H;
         const int hb0 = ns * (kNH / 32) + w * 2;   // this wave's first 32-unit block of W2^T
 
         // ---- 0. gather + patchify + bf16; e_t into LDS
-        for (int e = tid; e < kTok * kFeat; e += NT) {
-            const TokPos p = tok_pos(e, tb, d.Himg, d.Wimg);
-            xs[p.tl * kXRow + p.f] = (__bf16)xt[p.idx];
+        {
+            const float* xt = d.X + ((size_t)n * (d.T + 1) + min(t, ctrl->newest)) * d.D;   // beyond newest: its copy
+            const float* et = d.temb + (size_t)t * H;
+            for (int e = tid; e < kTok * kFeat; e += NT) {
+                const TokPos p = tok_pos(e, tb, d.Himg, d.Wimg);
+                xs[p.tl * kXRow + p.f] = (__bf16)xt[p.idx];
+            }
+            for (int i = tid; i < H / 4; i += NT)
+                reinterpret_cast<float4*>(es)[i] = reinterpret_cast<const float4*>(et)[i];
+            __syncthreads();
         }
-        for (int i = tid; i < H / 4; i += NT)
-            reinterpret_cast<float4*>(es)[i] = reinterpret_cast<const float4*>(et)[i];
-        __syncthreads();
 
         // ---- 1. h1 = GELU(x W1 + e_t): wave w computes units [32w, 32w + 32) of a chunk,
         // one 32-token slice per call, into LDS rows [token][unit].
@@ -168,31 +173,39 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
             ek = es + n0 + g * 4;
         };
         f32x16 h1acc;
+        // The accumulator starts at e_t (row = unit), so the MFMA returns x W1 + e_t; the
+        // GELU slices store 2 h1 (W2 is stored halved, see gelu2_erf).
         auto h1_mfma = [&](int tb4) {
             const bf16x8 b = *reinterpret_cast<const bf16x8*>(xs + (tb4 * 32 + l32) * kXRow + g * 8);
-            h1acc = mfma32(w1a, b, zero16);
+            f32x16 c0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 ev = *reinterpret_cast<const float4*>(ek + q * 8);
+                c0[q * 4 + 0] = ev.x;
+                c0[q * 4 + 1] = ev.y;
+                c0[q * 4 + 2] = ev.z;
+                c0[q * 4 + 3] = ev.w;
+            }
+            h1acc = mfma32(w1a, b, c0);
         };
-        auto h1_gelu = [&](__bf16* buf, int tb4, int q0) {   // units q0*8.. of the slice
+        auto h1_gelu = [&](__bf16* buf, int kc, int tb4, int q0) {   // units q0*8.. of the slice
             const int tok = tb4 * 32 + l32;
 #pragma unroll
             for (int q = q0; q < q0 + 2; ++q) {
-                const float4 ev = *reinterpret_cast<const float4*>(ek + q * 8);
                 bf16x4 v;
-                v[0] = (__bf16)gelu_erf(h1acc[q * 4 + 0] + ev.x);
-                v[1] = (__bf16)gelu_erf(h1acc[q * 4 + 1] + ev.y);
-                v[2] = (__bf16)gelu_erf(h1acc[q * 4 + 2] + ev.z);
-                v[3] = (__bf16)gelu_erf(h1acc[q * 4 + 3] + ev.w);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[i] = (__bf16)gelu2_erf(h1acc[q * 4 + i]);
                 *reinterpret_cast<bf16x4*>(buf + tok * HRow + w * 32 + q * 8 + g * 4) = v;
             }
         };
-        auto h1_slice = [&](__bf16* buf, int tb4) {
+        auto h1_slice = [&](__bf16* buf, int kc, int tb4) {
             h1_mfma(tb4);
-            h1_gelu(buf, tb4, 0);
-            h1_gelu(buf, tb4, 2);
+            h1_gelu(buf, kc, tb4, 0);
+            h1_gelu(buf, kc, tb4, 2);
         };
         h1_setup(0);
 #pragma unroll
-        for (int tb4 = 0; tb4 < 4; ++tb4) h1_slice(h1s[0], tb4);
+        for (int tb4 = 0; tb4 < 4; ++tb4) h1_slice(h1s[0], 0, tb4);
         __syncthreads();
 
         f32x16 acc2[2][4];
@@ -234,9 +247,9 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         // One chunk of GEMM2 (two register stages of W2^T fragments, the stream running on
         // across chunk boundaries). MORE: chunk kc + 1 exists; its h1 slices are computed
         // between the MFMA groups (same basic block, so the VALU work of the GELU can be
-        // interleaved with the MFMAs: kInterleave VALU instructions per MFMA). A wave raises
-        // its issue priority while it feeds MFMA groups, so that the two waves of a SIMD
-        // drift out of step (one in its MFMA group while the other is in its GELU slice).
+        // interleaved with the MFMAs). A wave raises its issue priority while it feeds MFMA
+        // groups, so that the two waves of a SIMD drift out of step (one in its MFMA group
+        // while the other is in its GELU slice).
         auto chunk = [&](int kc, auto more_c) {
             constexpr bool more = decltype(more_c)::value;
             if constexpr (more) h1_setup(kc + 1);
@@ -249,16 +262,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(1);
                 mma(A0, h1b, kb);
-                if constexpr (more) {
-                    h1_slice(nbuf, it);
-                    if constexpr (kInterleave > 0) {
-#pragma unroll
-                        for (int q = 0; q < 17; ++q) {
-                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                            __builtin_amdgcn_sched_group_barrier(0x002, kInterleave, 0);
-                        }
-                    }
-                }
+                if constexpr (more) h1_slice(nbuf, kc + 1, it);
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(0);
                 // Next fragments: this chunk's, or the first of the next chunk (after the
@@ -278,7 +282,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         for (int kc = 0; kc + 1 < KCH; ++kc) chunk(kc, std::true_type{});
         chunk(KCH - 1, std::false_type{});
 
-        // ---- 3. eps^T partial = W3p GELU(h2^T) straight from the accumulators
+        // ---- 3. eps^T partial = W3p GELU(h2^T) straight from the accumulators (2 GELU with W3
+        // stored halved)
         f32x16 acc3[4] = {zero16, zero16, zero16, zero16};
 #pragma unroll
         for (int hb = 0; hb < 2; ++hb) {
@@ -290,7 +295,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                 for (int tb4 = 0; tb4 < 4; ++tb4) {
                     bf16x8 b3;
 #pragma unroll
-                    for (int i = 0; i < 8; ++i) b3[i] = (__bf16)gelu_erf(acc2[hb][tb4][jj * 8 + i]);
+                    for (int i = 0; i < 8; ++i) b3[i] = (__bf16)gelu2_erf(acc2[hb][tb4][jj * 8 + i]);
                     acc3[tb4] = mfma32(a3, b3, acc3[tb4]);
                 }
             }
@@ -316,6 +321,12 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
             out[p.idx] = sum;
         }
         __syncthreads();                 // LDS is reused by the next item
+    };
+
+    for (int item = blockIdx.x; item < items; item += gridDim.x) {
+        const int ns = item % NS;
+        const int rest = item / NS;
+        half(rest / nblk, rest % nblk, ns);
     }
 }
 
