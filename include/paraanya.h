@@ -159,7 +159,9 @@ typedef struct {
     int64_t eps_latents;      /* latents evaluated by those launches (= nfe) */
     int64_t solver_launches;  /* Picard launches (= window-slide launches) */
     double  picard_ms_total;  /* summed durations of the drift / Picard / cache-update kernel */
-    double  slide_ms_total;   /* summed durations of the residual / slide / hit-test kernel */
+    double  slide_ms_total;   /* summed durations of the residual / slide / hit-test kernel
+                                 (0 for a fused handle, see paraanya_sweep: its slide runs in
+                                 the network kernel) */
 } pa_ktimes_t;
 
 /* ------------------------------------------------------------------ entry points */
@@ -197,7 +199,13 @@ PA_API int paraanya_set_revisit_threshold(paraanya_t* h, double threshold);
 /* Enqueue one sweep (steps (1)-(6) above) of every sample not yet done. If done != NULL
  * the stream is synchronized and *done receives 1 once every sample is done. Errors: STATE
  * (before reset, or the last synchronized state was already done), NONFINITE (only when
- * done != NULL and a residual was NaN/Inf). */
+ * done != NULL and a residual was NaN/Inf).
+ * A handle of one patch-MLP sample whose window's fp64 partial sums are small (2 P times the
+ * Picard kernel's D/64 column blocks, at most 256 KiB) runs its sweeps fused: the window
+ * slide of step (6) runs at the start of the next sweep's network kernel (every block
+ * computes it; one publishes it), and whenever the host reads the state (done != NULL,
+ * stats, trace, read_state) a finishing slide runs first, so every call observes the same
+ * state as with a separate slide kernel. */
 PA_API int paraanya_sweep(paraanya_t* h, int32_t* done);
 
 /* reset, sweeps until every sample is done, then x_out (device, N x D fp32) <- state T of

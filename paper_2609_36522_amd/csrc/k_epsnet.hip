@@ -33,6 +33,7 @@
 #include <hip/hip_ext.h>
 
 #include "pa_device.h"
+#include "pa_slide.h"
 
 namespace pa {
 
@@ -123,7 +124,37 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     // Misses per sample (0 once a sample is done), inclusive prefix over the samples.
     __shared__ int mpre[PA_MAX_BATCH + 1];
     static_assert(PA_MAX_BATCH <= 64, "one wave scans the samples");
-    if (w == 0) {
+    // Fused sweep (one sample): every block computes the outstanding window slide itself from
+    // the Picard kernel's snapshot and partial sums (block 0 publishes it), and keeps the miss
+    // list and the newest computed state in LDS; nothing this kernel writes is read back by it.
+    __shared__ int fmiss[PA_MAX_WINDOW];
+    __shared__ int fnewest;
+    if (d.fused_slide) {
+        const SlidePre pre = d.pre[0];
+        if (pre.pending) {
+            static_assert(sizeof(SlideScratch) + 16 + kSlideSubDoubles * sizeof(double) <= sizeof(h1s),
+                          "slide scratch must fit");
+            SlideScratch& sc = *reinterpret_cast<SlideScratch*>(&h1s[0][0]);
+            double* sub = reinterpret_cast<double*>(&h1s[0][0] + (sizeof(SlideScratch) + 15) / 16 * 8);
+            slide_core<NT>(d, 0, pre, blockIdx.x == 0, sc, sub);
+            const int m = sc.done ? 0 : sc.m;
+            for (int j = tid; j < m; j += NT) fmiss[j] = sc.miss_idx[j];
+            if (tid == 0) {
+                mpre[0] = 0;
+                mpre[1] = m;
+                fnewest = sc.newest;
+            }
+        } else {                             // first sweep after reset: the reset's window
+            const Ctrl* c = d.ctrl;
+            const int m = c->done ? 0 : c->m;
+            for (int j = tid; j < m; j += NT) fmiss[j] = c->miss_idx[j];
+            if (tid == 0) {
+                mpre[0] = 0;
+                mpre[1] = m;
+                fnewest = c->newest;
+            }
+        }
+    } else if (w == 0) {
         int v = 0;
         if (lane < d.N) v = d.ctrl[lane].done ? 0 : d.ctrl[lane].m;
 #pragma unroll
@@ -147,12 +178,13 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         while (mpre[n + 1] <= gm) ++n;               // sample of list entry gm (uniform)
         const int jm = gm - mpre[n];
         const Ctrl* ctrl = d.ctrl + n;
-        const int t = ctrl->miss_idx[jm];
+        const int t = d.fused_slide ? fmiss[jm] : ctrl->miss_idx[jm];
+        const int newest = d.fused_slide ? fnewest : ctrl->newest;
         const int hb0 = ns * (kNH / 32) + w * 2;   // this wave's first 32-unit block of W2^T
 
         // ---- 0. gather + patchify + bf16; e_t into LDS
         {
-            const float* xt = d.X + ((size_t)n * (d.T + 1) + min(t, ctrl->newest)) * d.D;   // beyond newest: its copy
+            const float* xt = d.X + ((size_t)n * (d.T + 1) + min(t, newest)) * d.D;   // beyond newest: its copy
             const float* et = d.temb + (size_t)t * H;
             for (int e = tid; e < kTok * kFeat; e += NT) {
                 const TokPos p = tok_pos(e, tb, d.Himg, d.Wimg);

@@ -28,6 +28,7 @@
 #include <hip/hip_ext.h>
 
 #include "pa_device.h"
+#include "pa_slide.h"
 
 namespace pa {
 
@@ -98,6 +99,7 @@ __global__ void k_reset(Dev d) {
         }
     }
     if (tid == 0) {
+        if (d.pre) d.pre[n].pending = 0;
         c->s = 0;
         c->e = W;
         c->newest = 0;
@@ -303,6 +305,8 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
         d.part_dev[pbase + tid * nblk + blockIdx.x] = rdev[tid];
         if (blockIdx.x == 0 && ctrl->slot_miss[tid]) d.valid[(size_t)n * d.T + s + tid] = 1;   // Eq. (7) entry
     }
+    // Fused sweep: the state this sweep started from, for the slide of the next network kernel.
+    if (d.fused_slide && blockIdx.x == 0 && tid == 0) d.pre[n] = slide_pre_of(*ctrl);
 }
 
 template <bool LINEAR, int NS>
@@ -330,159 +334,32 @@ hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t e0
 }
 
 // ---------------------------------------------------------------------------- slide
-// Residuals r of states s+1..e and deviations of states s+1..e-1 from the Picard partials
-// (one pass: thread (q, sub) sums the partials sub, sub + G, ... of reduction q, with the
-// loads independent; the G sub-sums meet in LDS in a fixed order). Then the Eq. (2) count
-// over s+1..e-1, the slide s' = s + 1 + c, done; then the next window's hit test and
-// compaction. Every barrier below is reached by all threads of the block.
+// One block per sample: the slide of its current state (FROM_PRE: of the Picard kernel's
+// snapshot, outstanding after a fused sweep; nothing to do if there is none).
+template <bool FROM_PRE>
 __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
     const int n = blockIdx.x;
-    Ctrl* ctrl = d.ctrl + n;
+    const Ctrl* ctrl = d.ctrl + n;
     if (ctrl->done) return;
-    pa_sweep_trace_t* const trace = d.trace ? d.trace + (size_t)n * d.T : nullptr;
-    const int s = ctrl->s, e = ctrl->e, W = e - s;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nblk = d.picard_blocks;
-    __shared__ double r_s[PA_MAX_WINDOW];
-    __shared__ double dv_s[PA_MAX_WINDOW];
-    __shared__ double sub_s[kSlideThreads];
-    __shared__ int wfirst[4];
-    __shared__ int wbad[4];
-    __shared__ int wcount[4];
-    __shared__ int wrev[4];
-    __shared__ int wbelow[4];
-    __shared__ int s_next;
-
-    const int NQ = 2 * W;                   // q < W: residual q; q >= W: deviation q - W
-    int G = 1;
-    while (G * 2 * NQ <= kSlideThreads) G *= 2;
-    {
-        const int q = tid / G, sub = tid - q * G;
-        double acc = 0.0;
-        if (q < NQ) {
-            const size_t pbase = (size_t)n * d.P * nblk;
-            const double* pr = (q < W) ? d.part_res + pbase + (size_t)q * nblk
-                                       : d.part_dev + pbase + (size_t)(q - W) * nblk;
-#pragma unroll 16
-            for (int b = sub; b < nblk; b += G) acc += pr[b];
-        }
-        sub_s[tid] = acc;
+    SlidePre pre;
+    if (FROM_PRE) {
+        pre = d.pre[n];
+        if (!pre.pending) return;
+    } else {
+        pre = slide_pre_of(*ctrl);
     }
-    __syncthreads();
-    if (tid < NQ) {
-        double v = 0.0;
-        for (int u = 0; u < G; ++u) v += sub_s[tid * G + u];
-        if (tid < W) r_s[tid] = v / (double)d.D;
-        else dv_s[tid - W] = v / (double)d.D;
-    }
-    __syncthreads();
-
-    // ---- Eq. (2): slot j stops the leading run if not converged or if it is the last slot.
-    {
-        const int j = tid;
-        const double r = j < W ? r_s[j] : 0.0;
-        const bool stop = (j < 256) && ((j >= W - 1) || !(r <= d.tol));
-        const bool bad = (j < W) && !isfinite(r);
-        const unsigned long long sm = __ballot(stop);
-        const unsigned long long bm = __ballot(bad);
-        if (wave < 4 && lane == 0) {
-            wfirst[wave] = sm ? wave * 64 + __ffsll((long long)sm) - 1 : 1 << 30;
-            wbad[wave] = bm != 0ull;
-        }
-        if (trace && j < W) trace[ctrl->sweep].resid[j] = r;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int c = 1 << 30, anybad = 0;
-        for (int w = 0; w < 4; ++w) {
-            c = min(c, wfirst[w]);
-            anybad |= wbad[w];
-        }
-        const int s2 = s + 1 + c;
-        if (anybad) ctrl->nonfinite = 1;
-        if (trace) {
-            pa_sweep_trace_t* rec = trace + ctrl->sweep;
-            rec->c = c;
-            rec->s_next = s2;
-            rec->sweep = ctrl->sweep;
-        }
-        ctrl->c = c;
-        ctrl->newest = max(ctrl->newest, e);
-        ctrl->s = s2;
-        ctrl->e = min(s2 + d.P, d.T);
-        ctrl->done = s2 >= d.T;
-        ctrl->sweep += 1;
-        s_next = s2;
-        // Progress word for the host's launch loop (pinned host memory, system scope; the
-        // host only reads this word and synchronizes the stream before reading anything else).
-        const uint64_t word = ((uint64_t)(uint32_t)ctrl->sweep << 32) |
-                              ((uint64_t)(s2 >= d.T) << 31) | (uint64_t)(uint32_t)min(s2, d.T);
-        __hip_atomic_store(d.progress + n, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    }
-    __syncthreads();
-    const int s2 = s_next;
-    if (s2 >= d.T) return;                  // uniform: every thread reads the same s_next
-
-    // ---- next window [s2, e2): Eq. (4)-(5) for slots that hold a cache entry (t < e); first
-    // entries (t >= e) are misses; compaction by wave ballots and LDS offsets.
-    const int e2 = min(s2 + d.P, d.T), W2 = e2 - s2;
-    const int next = ctrl->sweep;           // index of the next sweep (set above by tid 0)
-    const int j = tid, t = s2 + j;
-    double dev = __builtin_nan("");
-    bool hit = false, miss = false, rev = false, below = false;
-    if (j < W2) {
-        if (t < e) {
-            dev = dv_s[t - s - 1];
-            hit = dev < d.delta;            // strict: delta == 0 never hits
-            rev = true;                     // t holds a cache entry: a revisit
-            below = dev < d.revisit_thr;
-        }
-        miss = !hit;
-    }
-    const unsigned long long mask = __ballot(miss);
-    const unsigned long long rmask = __ballot(rev);
-    const unsigned long long bmask = __ballot(below);
-    const int rank = __popcll(mask & lanemask_lt());
-    if (wave < 4 && lane == 0) {
-        wcount[wave] = __popcll(mask);
-        wrev[wave] = __popcll(rmask);
-        wbelow[wave] = __popcll(bmask);
-    }
-    __syncthreads();
-    if (j < 256) {
-        int off = 0;
-        for (int w = 0; w < wave; ++w) off += wcount[w];
-        const int m = wcount[0] + wcount[1] + wcount[2] + wcount[3];
-        if (miss) ctrl->miss_idx[off + rank] = t;
-        if (j < W2) {
-            ctrl->slot_miss[j] = miss ? 1 : 0;
-            ctrl->slot_rank[j] = miss ? (uint8_t)(off + rank) : 0;
-        }
-        if (trace) {
-            pa_sweep_trace_t* rec = trace + next;
-            if (j < W2) {
-                rec->dev[j] = dev;
-                rec->hit[j] = hit ? 1 : 0;
-            }
-            if (miss) rec->miss_idx[off + rank] = t;
-            if (tid == 0) {
-                rec->s = s2;
-                rec->e = e2;
-                rec->m = m;
-            }
-        }
-        if (tid == 0) {
-            ctrl->m = m;
-            ctrl->nfe += m;
-            ctrl->hits += W2 - m;
-            ctrl->revisits += wrev[0] + wrev[1] + wrev[2] + wrev[3];
-            ctrl->revisits_below += wbelow[0] + wbelow[1] + wbelow[2] + wbelow[3];
-        }
-    }
+    __shared__ SlideScratch sc;
+    __shared__ double sub[kSlideSubDoubles];
+    slide_core<kSlideThreads>(d, n, pre, true, sc, sub);
 }
 
 hipError_t launch_slide(const Dev& d, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-    hipExtLaunchKernelGGL(k_slide, dim3(d.N), dim3(kSlideThreads), 0, st, e0, e1, 0, d);
+    hipExtLaunchKernelGGL(k_slide<false>, dim3(d.N), dim3(kSlideThreads), 0, st, e0, e1, 0, d);
+    return hipGetLastError();
+}
+
+hipError_t launch_slide_pending(const Dev& d, hipStream_t st) {
+    hipLaunchKernelGGL(k_slide<true>, dim3(d.N), dim3(kSlideThreads), 0, st, d);
     return hipGetLastError();
 }
 

@@ -28,6 +28,14 @@ struct alignas(256) Ctrl {
     uint8_t slot_rank[PA_MAX_WINDOW]; // per miss slot j: its position in miss_idx
 };
 
+// The control-block fields the window slide reads, as they were before it (the fused sweep's
+// Picard kernel leaves this snapshot for the slide that the next network kernel computes).
+struct SlidePre {
+    int32_t s, e, newest, sweep, nonfinite;
+    int32_t pending;    // a slide of this state is outstanding (0 right after reset)
+    int64_t nfe, hits, revisits, revisits_below;
+};
+
 // Geometry and device buffers handed to every kernel launcher. Per-sample buffers are
 // stacked along a leading sample index n < N.
 struct Dev {
@@ -47,6 +55,8 @@ struct Dev {
     double* part_res;          // [N][P][picard_blocks] fp64 partial sums of Eq. (2) residuals
     double* part_dev;          // [N][P][picard_blocks] fp64 partial sums of Eq. (4) deviations
     Ctrl* ctrl;                // [N]
+    SlidePre* pre;             // [N] pre-slide snapshots (fused sweep), or null
+    int32_t fused_slide;       // 1: the network kernel computes the slide (N = 1), no k_slide
     uint64_t* progress;        // [N] host-mapped words: sweeps << 32 | done << 31 | s
     pa_sweep_trace_t* trace;   // [N][T] or null
     // patch-MLP weights in device layouts
@@ -70,6 +80,10 @@ struct Dev {
 hipError_t launch_reset(const Dev& d, hipStream_t st);
 // start/stop: optional events attached to the kernel's dispatch (null = untimed).
 hipError_t launch_slide(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop);
+// The slide outstanding after a fused sweep, from the Picard kernel's snapshot (no-op if none).
+hipError_t launch_slide_pending(const Dev& d, hipStream_t st);
+// Largest fp64 partial-sum volume per sample the network kernel reduces redundantly per block.
+constexpr size_t kFusedSlideMaxBytes = 256 * 1024;
 hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_temb_table(const Dev& d, const double* t_values_dev, const __bf16* wt_dev,

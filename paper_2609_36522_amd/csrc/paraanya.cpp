@@ -32,6 +32,7 @@ struct paraanya {
     pa::DevMem mem;                   // device allocations
     pa::KernelTimer timer;            // kinds: 0 network, 1 Picard, 2 slide
     int64_t timed_latents = 0;        // network latents of the samples the timer covers
+    bool slide_pending = false;       // fused sweep: the last sweep's slide is not computed yet
 
     ~paraanya() {
         (void)hipStreamSynchronize(stream);
@@ -45,6 +46,12 @@ struct paraanya {
     int read_ctrl() {
         // The mirror stays valid until the next enqueue, so repeated queries cost nothing.
         if (ctrl_fresh) return PA_OK;
+        if (slide_pending) {
+            // Fused sweep: bring the control block up to date (the next network kernel computes
+            // the same slide again and writes the same values).
+            PA_HIP(pa::launch_slide_pending(d, stream));
+            slide_pending = false;
+        }
         PA_HIP(hipMemcpyAsync(ctrl_host, d.ctrl, (size_t)d.N * sizeof(Ctrl), hipMemcpyDeviceToHost, stream));
         PA_HIP(hipStreamSynchronize(stream));
         host_done = true;
@@ -80,6 +87,12 @@ struct paraanya {
         }
         if ((rc = timed(1, &e0, &e1))) return rc;
         PA_HIP(pa::launch_picard(d, stream, model == PA_EPS_LINEAR, e0, e1));
+        if (d.fused_slide) {
+            // The slide runs at the start of the next network kernel (or of a finishing
+            // k_slide when the host needs the control block first).
+            slide_pending = true;
+            return PA_OK;
+        }
         if ((rc = timed(2, &e0, &e1))) return rc;
         PA_HIP(pa::launch_slide(d, stream, e0, e1));
         return PA_OK;
@@ -163,6 +176,11 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     if ((rc = h->alloc(&d.part_res, Nz * window * d.picard_blocks, "part_res"))) return bail(rc);
     if ((rc = h->alloc(&d.part_dev, Nz * window * d.picard_blocks, "part_dev"))) return bail(rc);
     if ((rc = h->alloc(&d.ctrl, Nz, "ctrl"))) return bail(rc);
+    // Fused sweep (network -> Picard, the slide computed by every block of the next network
+    // kernel): one sample, patch-MLP, and a partial-sum volume that a block reduces quickly.
+    d.fused_slide = (em->kind == PA_EPS_PATCH_MLP && N == 1 &&
+                     2 * (size_t)window * d.picard_blocks * sizeof(double) <= pa::kFusedSlideMaxBytes) ? 1 : 0;
+    if ((rc = h->alloc(&d.pre, Nz, "pre"))) return bail(rc);
     if (flags & PA_FLAG_TRACE)
         if ((rc = h->alloc(&d.trace, Nz * T, "trace"))) return bail(rc);
     if (eta > 0.0) {
@@ -204,6 +222,7 @@ int paraanya_reset(paraanya_t* h, const float* x_init) {
     PA_HIP(hipMemcpy2DAsync(h->d.X, (size_t)(h->d.T + 1) * row, x_init, row, row, (size_t)h->d.N,
                             hipMemcpyDeviceToDevice, h->stream));
     PA_HIP(pa::launch_reset(h->d, h->stream));
+    h->slide_pending = false;
     h->have_reset = true;
     h->host_done = false;
     return PA_OK;
@@ -248,14 +267,15 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
     int rc = paraanya_reset(h, x_init);
     if (rc) return rc;
     const int T = h->d.T, P = h->d.P, N = h->d.N;
-    // Launch loop without per-sweep synchronisation: k_slide publishes (completed sweeps,
-    // done, s) of every sample to a pinned host word after each sweep; the host keeps enough
-    // sweeps in flight -- at least the kLookahead next ones and at least the ceil((T - s)/P)
-    // that the slowest sample certainly still needs (s advances by at most P per sweep) --
-    // and stops enqueuing once every sample is done. Sweeps enqueued after that exit at
-    // their first instruction. Every sweep advances each unfinished sample's s by at least 1,
-    // so at most T sweeps are ever enqueued. The stream is polled while waiting, so a failed
-    // or idle stream ends the loop.
+    // Launch loop without per-sweep synchronisation: the window slide (k_slide, or the next
+    // network kernel in a fused sweep) publishes (completed sweeps, done, s) of every sample to
+    // a pinned host word after each sweep; the host keeps enough sweeps in flight -- at least
+    // the kLookahead next ones and at least the ceil((T - s)/P) that the slowest sample
+    // certainly still needs (s advances by at most P per sweep) -- and stops enqueuing once
+    // every sample is done. Sweeps enqueued after that exit at their first instruction. Every
+    // sweep advances each unfinished sample's s by at least 1, so at most T sweeps are ever
+    // enqueued (T + 1 for a fused sweep, see below). The stream is polled while waiting, so a
+    // failed or idle stream ends the loop.
     constexpr int kLookahead = 2;
     volatile uint64_t* prog = h->progress_host;
     auto scan = [&](int* completed, int* need) {      // returns true once all are done
@@ -273,13 +293,16 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
         }
         return all;
     };
+    // A fused sweep's slide runs in the next sweep's network kernel, so the sweep that finishes
+    // the sample is followed by one more (its network kernel only computes that slide).
+    const int cap = T + (h->d.fused_slide ? 1 : 0);
     int enqueued = 0;
     for (unsigned spin = 0;; ++spin) {
         int completed, need;
         if (scan(&completed, &need)) break;
         const int want = completed + (need > kLookahead ? need : kLookahead);
-        if (enqueued < want && enqueued < T) {
-            const int k = (want < T ? want : T) - enqueued;
+        if (enqueued < want && enqueued < cap) {
+            const int k = (want < cap ? want : cap) - enqueued;
             for (int i = 0; i < k; ++i)
                 if ((rc = h->enqueue_sweep())) return rc;
             enqueued += k;
@@ -290,12 +313,14 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
         if (q == hipSuccess) {
             // Stream idle: the words are final for the enqueued work.
             if (scan(&completed, &need)) break;
-            if (enqueued >= T) return fail(PA_ERR_HIP, "sampler did not finish within T sweeps");
+            if (enqueued >= cap) return fail(PA_ERR_HIP, "sampler did not finish within T sweeps");
         } else if (q != hipErrorNotReady) {
             return hip_fail(q, "hipStreamQuery");
         }
     }
-    // One synchronization for the output copy and the counters.
+    // Every sample is done: the slide that published that also wrote the control block, so no
+    // finishing slide is needed. One synchronization for the output copy and the counters.
+    h->slide_pending = false;
     const size_t row = (size_t)h->d.D * sizeof(float);
     PA_HIP(hipMemcpy2DAsync(x_out, row, h->d.X + (size_t)T * h->d.D, (size_t)(T + 1) * row, row,
                             (size_t)N, hipMemcpyDeviceToDevice, h->stream));

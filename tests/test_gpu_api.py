@@ -19,7 +19,12 @@ def _x(wl, seed=0):
     return torch.from_numpy(inputs.x_init(wl.latent, seed).reshape(-1)).cuda()
 
 
-@pytest.mark.parametrize("wl", [W.TINY_LINEAR, W.SMALL_MLP], ids=["linear", "mlp"])
+# mlp_window1: a fused patch-MLP handle whose sample needs exactly T sweeps (window 1), so its
+# last slide runs in a network kernel launched after the T-th sweep.
+@pytest.mark.parametrize("wl", [W.TINY_LINEAR, W.SMALL_MLP,
+                                W.Workload("mlp_4x16x32_T6_P1", (4, 16, 32), 6, 1, 0.05, 1e-3,
+                                           "patch_mlp", hidden=512)],
+                         ids=["linear", "mlp", "mlp_window1"])
 def test_sample_equals_sweep_by_sweep_and_is_deterministic(wl, gpu_lib):
     x = _x(wl)
     with B.from_workload(wl, trace=True) as s:
@@ -36,6 +41,8 @@ def test_sample_equals_sweep_by_sweep_and_is_deterministic(wl, gpu_lib):
         X, _, _, _ = s.read_state(wl.T, wl.T + 1)
     assert np.array_equal(out1, out2) and np.array_equal(out1, X[0])
     assert st1 == st2 == st3
+    if wl.window == 1:
+        assert st1["sweeps"] == wl.T
     for a, b in zip(tr1, tr2):
         assert a["miss"] == b["miss"] and a["c"] == b["c"]
         assert np.array_equal(a["dev"], b["dev"], equal_nan=True) and np.array_equal(a["r"], b["r"])
@@ -128,6 +135,13 @@ def test_profile_counts_launches(gpu_lib):
         s.sample(_x(wl))
         kt = s.kernel_times()
     assert kt["solver_launches"] == kt["launches"] >= st["sweeps"]
+    # One patch-MLP sample: the window slide runs inside the next network kernel (no k_slide).
+    assert kt["picard_ms_total"] > 0 and kt["slide_ms_total"] == 0.0
+    with B.from_workload(wl, profile_solver=True, batch=2) as s:
+        xs = torch.from_numpy(inputs.x_init_batch(wl.latent, 2).reshape(-1)).cuda()
+        s.sample(xs)
+        kt = s.kernel_times()
+    assert kt["solver_launches"] == kt["launches"] > 0
     assert kt["picard_ms_total"] > 0 and kt["slide_ms_total"] > 0
 
 
