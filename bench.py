@@ -168,7 +168,10 @@ def solver_kernels(r, D):
     return {"k_picard": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": (gbs / PEAK_HBM_GBS) if gbs else None,
                          "bytes_per_launch": byts / n, "avg_launch_us": 1e3 * r["picard_ms"] / n},
-            "k_slide": {"bound": "latency", "avg_launch_us": 1e3 * r["slide_ms"] / n}}
+            "k_slide": ({"bound": "latency", "avg_launch_us": 1e3 * r["slide_ms"] / n}
+                        if r["slide_ms"] > 0 else
+                        {"fused": "computed at the start of the next network kernel (one "
+                                  "patch-MLP sample): no launch of its own"})}
 
 
 def run_case(wl, delta, steps, warmup, torch, weights, *, batch=1, eta=0.0, solver=False):
