@@ -147,6 +147,10 @@ int picard_blocks(int D) { return (D / 4 + kCols - 1) / kCols; }
 // fixed-order sum of the network kernel's partial outputs.
 // NS: partial outputs per fresh network output (the network kernel's splits of the output
 // units; 1 for the linear network).
+// Zero vectors as values: a named local zero vector was kept in scratch memory by the compiler.
+__device__ __forceinline__ float4 f4_zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+__device__ __forceinline__ double4 d4_zero() { return make_double4(0.0, 0.0, 0.0, 0.0); }
+
 template <int TPT, bool LINEAR, int NS>
 __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     const int n = blockIdx.y;
@@ -164,8 +168,6 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     float* Xh = d.Xh + (size_t)n * d.T * D;
     float* Eh = d.Eh + (size_t)n * d.T * D;
     const float* noise = d.noise ? d.noise + (size_t)n * d.T * D : nullptr;
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-    const double4 dzero = make_double4(0.0, 0.0, 0.0, 0.0);
 
     // ---- the states (independent of the miss list) first; meanwhile the block stages the
     // per-slot miss flags and ranks in LDS, so that the address of every other load is known
@@ -174,12 +176,12 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     // slot j0 + k and the previous iterate of the state slot j0 + k - 1 updates.
     float4 xs[TPT + 1], e0[TPT], ex[TPT][NS > 1 ? NS - 1 : 1], zt[TPT], xhn[TPT];
     double cf[TPT][3];
-    float4 anchor = zero;
+    float4 anchor = f4_zero();
     if (colok) anchor = reinterpret_cast<const float4*>(X + min(s, newest) * D)[c4];
 #pragma unroll
     for (int k = 0; k <= TPT; ++k) {
         const int j = j0 + k;
-        xs[k] = (j <= W && colok) ? reinterpret_cast<const float4*>(X + min(s + j, newest) * D)[c4] : zero;
+        xs[k] = (j <= W && colok) ? reinterpret_cast<const float4*>(X + min(s + j, newest) * D)[c4] : f4_zero();
     }
     __shared__ uint8_t sm[PA_MAX_WINDOW + TPT + 1];
     __shared__ uint8_t sr[PA_MAX_WINDOW + TPT];
@@ -203,11 +205,11 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
         const int j = j0 + k, t = s + j;
         const bool act = j < W && colok;
         const bool miss = f[k] != 0;
-        e0[k] = zero;
-        zt[k] = zero;
-        xhn[k] = zero;
+        e0[k] = f4_zero();
+        zt[k] = f4_zero();
+        xhn[k] = f4_zero();
 #pragma unroll
-        for (int h = 0; h < (NS > 1 ? NS - 1 : 1); ++h) ex[k][h] = zero;
+        for (int h = 0; h < (NS > 1 ? NS - 1 : 1); ++h) ex[k][h] = f4_zero();
         cf[k][0] = cf[k][1] = cf[k][2] = 0.0;
         if (act) {
             // Eq. (6): the cached output of a hit, or the network kernel's partial outputs of
@@ -236,7 +238,7 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
         const int j = j0 + k, t = s + j;
-        dr[k] = dzero;
+        dr[k] = d4_zero();
         if (j + 1 < W && f[k + 1]) xhn[k] = xs[k + 1];
         if (j < W && colok) {
             const float4 x = xs[k];
