@@ -21,10 +21,14 @@ Beside the headline line (same JSON object, extra keys):
 Prints one JSON line (rank 0). Throughput figures (value, ms_per_step, ε evals/s, and those of
 the extra measurements) come from samples launched exactly as a user launches them, with no
 timing events. Kernel durations come from a second pass over the same samples on a handle
-whose network launches carry start/stop HIP events on the sampler's stream (the events add
-stream time, so that pass is not the throughput). The roofline object describes the dominant
-kernel (the fused patch-MLP network kernel): achieved = algorithmic FLOPs of its launches /
-their summed event-timed duration.
+whose network launches carry start/stop HIP events attached to their dispatches on the
+sampler's stream (the events add stream time, so that pass is not the throughput). An event
+pair can include idle time before its kernel on the stream: without a profiler attached the
+event-timed network duration is within about 1% of rocprofv3's kernel duration, while a
+profiler spaces the kernels further apart and the event figure of a profiled run grows with
+it. The roofline object describes the
+dominant kernel (the fused patch-MLP network kernel): achieved = algorithmic FLOPs of its
+launches / their summed event-timed duration.
 """
 from __future__ import annotations
 
@@ -416,7 +420,7 @@ def main():
                      "avg_launch_us": 1e3 * p["eps_ms"] / max(p["launches"], 1),
                      "flops_per_launch": p["profiled_nfe"] * fpe / max(p["launches"], 1),
                      "timing": "kernel durations from a second pass of the timed samples with "
-                               "start/stop events on every network launch"},
+                               "start/stop events attached to every network launch"},
     }
     line.update(extras)
     if not args.headline_only:

@@ -152,7 +152,9 @@ typedef struct {
 } pa_sweep_trace_t;
 
 /* Device time of the kernels since reset (PA_FLAG_PROFILE): each launch carries start/stop
- * events on the handle's stream. */
+ * events attached to its dispatch on the handle's stream. A pair can also cover idle time
+ * between the kernel and the work before it on the stream (little without a profiler
+ * attached, more under one, which spaces the kernels further apart). */
 typedef struct {
     int64_t launches;         /* network launches */
     double  eps_ms_total;     /* summed kernel durations of the network launches */

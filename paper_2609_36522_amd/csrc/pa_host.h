@@ -58,7 +58,8 @@ struct DevMem {
 };
 
 // Start/stop event pairs attached to kernel dispatches (hipExtLaunchKernelGGL), summed per
-// kernel kind when drained.
+// kernel kind when drained. A pair's interval can include idle time between the kernel and
+// the work before it on the stream.
 struct KernelTimer {
     static constexpr int kKinds = 3;
     std::vector<hipEvent_t> pool;
