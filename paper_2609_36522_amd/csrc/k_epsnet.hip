@@ -186,12 +186,26 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         {
             const float* xt = d.X + ((size_t)n * (d.T + 1) + min(t, newest)) * d.D;   // beyond newest: its copy
             const float* et = d.temb + (size_t)t * H;
-            for (int e = tid; e < kTok * kFeat; e += NT) {
-                const TokPos p = tok_pos(e, tb, d.Himg, d.Wimg);
-                xs[p.tl * kXRow + p.f] = (__bf16)xt[p.idx];
+            // Every load of the thread is issued before the first LDS store, so the block waits
+            // for one round trip to memory instead of one per element.
+            constexpr int kPer = kTok * kFeat / NT;
+            static_assert(kPer * NT == kTok * kFeat, "one element per thread and round");
+            constexpr int kEs = (H / 4 + NT - 1) / NT;
+            float xv[kPer];
+            float4 ev[kEs];
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) xv[k] = xt[tok_pos(tid + k * NT, tb, d.Himg, d.Wimg).idx];
+#pragma unroll
+            for (int k = 0; k < kEs; ++k)
+                if (tid + k * NT < H / 4) ev[k] = reinterpret_cast<const float4*>(et)[tid + k * NT];
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) {
+                const TokPos p = tok_pos(tid + k * NT, tb, d.Himg, d.Wimg);
+                xs[p.tl * kXRow + p.f] = (__bf16)xv[k];
             }
-            for (int i = tid; i < H / 4; i += NT)
-                reinterpret_cast<float4*>(es)[i] = reinterpret_cast<const float4*>(et)[i];
+#pragma unroll
+            for (int k = 0; k < kEs; ++k)
+                if (tid + k * NT < H / 4) reinterpret_cast<float4*>(es)[tid + k * NT] = ev[k];
             __syncthreads();
         }
 
@@ -343,16 +357,31 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         }
         __syncthreads();
 
-        // ---- 4. fixed-order sum over waves, unpatchify, store this half's partial output
+        // ---- 4. fixed-order sum over waves, unpatchify, store this half's partial output.
+        // Thread = (channel c, token tl): its four features c*4 + dh*2 + dw are contiguous in
+        // the reduction buffer and form two float2 pairs (dw = 0, 1) in rows 2hp and 2hp + 1.
         float* out = d.Ep + (((size_t)ns * d.N + n) * d.P + jm) * d.D;
-        for (int e = tid; e < kTok * kFeat; e += NT) {
-            const TokPos p = tok_pos(e, tb, d.Himg, d.Wimg);
-            float sum = 0.f;
+        static_assert(kTok * (kFeat / 4) == NT, "one token and channel per thread");
+        {
+            const int tl = tid & (kTok - 1), c = tid / kTok;
+            float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-            for (int ww = 0; ww < kWaves; ++ww) sum += red[((size_t)ww * kTok + p.tl) * kFeat + p.f];
-            out[p.idx] = sum;
+            for (int ww = 0; ww < kWaves; ++ww) {
+                const float4 v = *reinterpret_cast<const float4*>(red + ((size_t)ww * kTok + tl) * kFeat + c * 4);
+                sum.x += v.x;
+                sum.y += v.y;
+                sum.z += v.z;
+                sum.w += v.w;
+            }
+            const int half_w = d.Wimg >> 1;
+            const int tok = tb * kTok + tl;
+            const int hp = tok / half_w, wp = tok - hp * half_w;
+            float* o = out + ((size_t)c * d.Himg + 2 * hp) * d.Wimg + 2 * wp;
+            *reinterpret_cast<float2*>(o) = make_float2(sum.x, sum.y);
+            *reinterpret_cast<float2*>(o + d.Wimg) = make_float2(sum.z, sum.w);
         }
-        __syncthreads();                 // LDS is reused by the next item
+        // No barrier: the next item's gather writes xs and es only, and its barrier comes
+        // before anything overwrites the reduction buffer (the h1 buffers).
     };
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
