@@ -17,6 +17,9 @@ Beside the headline line (same JSON object, extra keys):
                      window of 64 on the same latent and network, delta in {0, 0.05}.
   parareal           the Parareal-style cached sampler: 4x96x96 latent, T = 100 in 10 blocks,
                      patch-MLP H = 2048 over 2304 tokens, delta in {0, 0.05}.
+  picard_beyond_cache  the solver kernels at 64 samples per handle of the same workload: one
+                     Picard launch then touches ~0.5 GB, more than the 256 MB Infinity Cache,
+                     so its rate is that of HBM (the one- and eight-sample figures are not).
 
 Prints one JSON line (rank 0). Throughput figures (value, ms_per_step, ε evals/s, and those of
 the extra measurements) come from samples launched exactly as a user launches them, with no
@@ -49,15 +52,16 @@ PRIMARY_DELTA = 0.05
 
 
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_eps_mlp_traffic_sd_4x64x64_T100_P32_H1024.md")
+PICARD64_RECORD = os.path.join(ROOT, "profiles", "k_picard_batched64_sd_4x64x64_T100_P32_H1024.md")
 
 
-def measured_traffic():
-    """HBM bytes per launch of the network kernel from the committed counter summary, or None
-    when the kernel sources changed since the counters were taken."""
+def measured_traffic(record=TRAFFIC_RECORD):
+    """HBM bytes per launch of a kernel from a committed counter summary, or None when the
+    kernel sources changed since the counters were taken."""
     import hashlib
     import re
     try:
-        text = open(TRAFFIC_RECORD).read()
+        text = open(record).read()
         rec = json.loads(re.search(r"```json\n(.*?)```", text, re.S).group(1))
         h = hashlib.sha256()
         for src in rec["sources"]:
@@ -84,7 +88,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--headline-only", action="store_true",
                     help="skip the revisit, batched, DDPM and Parareal measurements")
-    ap.add_argument("--extras", type=str, default="revisit,batched,ddpm,parareal",
+    ap.add_argument("--extras", type=str, default="revisit,batched,ddpm,parareal,hbm",
                     help="which extra measurements to run (comma list)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle's bounded sample")
@@ -320,6 +324,20 @@ def main():
                 run_case(wl, PRIMARY_DELTA, 3, 1, torch, weights, batch=nb, solver=True), wl.D)}
         print(f"[bench] batch {nb}: {extras['batched']['ms_per_batch']:.3f} ms/batch, "
               f"{extras['batched']['samples_per_s']:.0f} samples/s", file=sys.stderr, flush=True)
+    if not args.headline_only and "hbm" in want:
+        # Picard launches whose touched set exceeds the Infinity Cache
+        nh = 64
+        rh = run_case(wl, PRIMARY_DELTA, 2, 1, torch, weights, batch=nh, solver=True)
+        sk = solver_kernels(rh, wl.D)
+        traffic = measured_traffic(PICARD64_RECORD)
+        sk["k_picard"]["traffic"] = traffic
+        sk["k_picard"]["traffic_unit"] = "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
+        if traffic is not None:
+            sk["k_picard"]["traffic_GBps"] = traffic / (sk["k_picard"]["avg_launch_us"] * 1e-6) / 1e9
+        extras["picard_beyond_cache"] = {
+            "samples": nh, "delta": PRIMARY_DELTA, "steps": 2, "solver_kernels": sk}
+        print(f"[bench] picard at batch {nh}: {sk['k_picard']['bytes_per_launch'] / 1e6:.0f} MB/launch, "
+              f"{sk['k_picard']['achieved']:.0f} GB/s", file=sys.stderr, flush=True)
     if not args.headline_only and "ddpm" in want:
         # the window study's stochastic setting
         wd = wl.with_(T=1000, window=64)
