@@ -165,12 +165,14 @@ def solver_kernels(r, D):
     handle times them: their events add stream time, so it is not the headline run).
 
     k_picard's algorithmic bytes per sweep are the Picard update's (3W + 1) * 4D (read the
-    W + 1 window states and the W assembled outputs, write W states) plus 8D per miss (the
-    Eq. (7) cache writes of input and output); the cache-test re-reads it avoids are not
-    counted. Summed over a run: 4D * (3 * (nfe + hits) + sweeps + 2 * nfe). k_slide moves
-    only the fp64 partial sums and the control block: it is bound by latency, not bytes."""
+    W + 1 window states and the W assembled outputs, write W states) plus 4D per miss (the
+    Eq. (7) cache write of its input). Not counted: the Eq. (7) write of the fresh output (the
+    network kernel's whole outputs land in the cache directly; only launches with split
+    outputs leave it to k_picard), and the cache inputs of hit slots it reads for the next
+    sweep's Eq. (4) test. Summed over a run: 4D * (3 * (nfe + hits) + sweeps + nfe). k_slide
+    moves only the fp64 partial sums and the control block: it is bound by latency."""
     byts = 4.0 * D * (3 * (r["profiled_nfe"] + r["profiled_hits"]) + r["profiled_sweeps"]
-                      + 2 * r["profiled_nfe"])
+                      + r["profiled_nfe"])
     n = max(r["solver_launches"], 1)
     gbs = byts / (r["picard_ms"] * 1e-3) / 1e9 if r["picard_ms"] > 0 else None
     return {"k_picard": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",

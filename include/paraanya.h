@@ -115,6 +115,11 @@ typedef struct {
 #define PA_FLAG_PROFILE 2u   /* time every network launch with HIP events (paraanya_kernel_times) */
 #define PA_FLAG_PROFILE_SOLVER 4u  /* with PA_FLAG_PROFILE: time the Picard and slide launches
                                       too (their events add ~7 us per sweep of stream time) */
+#define PA_FLAG_SPLIT_OUTPUTS 8u   /* test hook (patch-MLP): every network launch writes split
+                                      partial outputs that the Picard kernel sums, instead of
+                                      choosing whole outputs written straight into the cache
+                                      when they cost no extra time; the results are the same
+                                      bit for bit either way */
 
 typedef struct paraanya paraanya_t;
 

@@ -33,6 +33,7 @@ PA_EPS_PATCH_MLP = 1
 PA_FLAG_TRACE = 1
 PA_FLAG_PROFILE = 2
 PA_FLAG_PROFILE_SOLVER = 4
+PA_FLAG_SPLIT_OUTPUTS = 8
 
 EXPORTED = ("paraanya_create", "paraanya_reset", "paraanya_sweep", "paraanya_sample",
             "paraanya_stats", "paraanya_trace", "paraanya_read_state", "paraanya_coefficients",
@@ -208,11 +209,12 @@ class Sampler:
     bit-pattern arrays w1, wt, w2, w3). ``batch`` independent samples share the handle
     (tensors passed to reset/sample hold batch x D values). ``eta`` > 0 selects the
     stochastic step (1 = ancestral DDPM); its step noise is given with :meth:`set_noise`.
-    ``stream`` is a torch.cuda.Stream or None (the current stream)."""
+    ``stream`` is a torch.cuda.Stream or None (the current stream). ``split_outputs`` (test
+    hook) keeps the network's outputs split over its partial buffers on every launch."""
 
     def __init__(self, latent, T, window, delta, tol, model, *, c=None, weights=None,
                  hidden=0, schedule=None, stream=None, trace=False, profile=False, batch=1,
-                 eta=0.0, profile_solver=False):
+                 eta=0.0, profile_solver=False, split_outputs=False):
         import torch
         self.lib = load_library()
         self.latent = tuple(int(v) for v in latent)
@@ -225,7 +227,8 @@ class Sampler:
         self._keep = []
         sc, em = _schedule_and_model(self._keep, schedule, eta, model, c, weights, hidden)
         flags = (PA_FLAG_TRACE if trace else 0) | (PA_FLAG_PROFILE if profile else 0) | \
-            (PA_FLAG_PROFILE | PA_FLAG_PROFILE_SOLVER if profile_solver else 0)
+            (PA_FLAG_PROFILE | PA_FLAG_PROFILE_SOLVER if profile_solver else 0) | \
+            (PA_FLAG_SPLIT_OUTPUTS if split_outputs else 0)
         h = C.c_void_p()
         _check(self.lib.paraanya_create(shape, self.T, C.byref(sc), self.P, float(delta),
                                         float(tol), C.byref(em), C.c_void_p(self.stream.cuda_stream),

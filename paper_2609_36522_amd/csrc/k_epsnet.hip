@@ -12,14 +12,22 @@
 //   2. h2^T += W2^T h1^T chunk by chunk: each of the 8 waves owns 64 output units x 128
 //      tokens (128 accumulator registers); W2^T fragments stream from L2 in MFMA-fragment
 //      order (1 KB contiguous per wave load), two register stages in flight; the GEMM1 and
-//      GELU of chunk c + 1 are computed between the MFMA groups of chunk c;
+//      GELU of the next chunk are computed between the MFMA groups of the current one;
 //   3. eps^T = W3^T GELU(h2^T), MFMA fed straight from the GEMM2 accumulators (reduction
 //      index permuted to the accumulator layout; W3 stored pre-permuted);
-//   4. per-wave partials summed in a fixed order through LDS, unpatchified, written as this
-//      half's partial output; the Picard kernel adds the halves in a fixed order and writes
-//      the cache.
+//   4. per-wave partials summed in a fixed order through LDS and unpatchified.
+// Two ways to finish (chosen per launch from the miss count, identically in every block,
+// by the time each takes):
+//   split outputs: each item is a work item of its own and writes its half's partial output;
+//      the Picard kernel adds the halves in a fixed order and writes the cache;
+//   whole outputs (at most two halves): one block runs both halves of a token block in turn,
+//      adds their outputs in the same fixed order and writes the fresh output straight into
+//      the cache (Eq. (6)-(7), output side). The second half takes its K-chunks in the order
+//      2, 3, 1, 0 (generally H/256 - 2, H/256 - 1, H/256 - 3, ..., 0), so the first of them is
+//      the h1 chunk the first half left in LDS: no gather, no h1 prologue, one chunk of GELU
+//      work less. Odd halves take that order in both ways, so both give the same bits.
 // 128 tokens per item make every W2 byte feed 128 FLOP, which keeps the W2 stream under the
-// per-CU vector-memory bandwidth; the price is computing h1 once per half.
+// per-CU vector-memory bandwidth; the price is computing h1 (largely) once per half.
 // All products are bf16 x bf16 with fp32 accumulation.
 //
 // Accumulator layout of v_mfma_f32_32x32x16_bf16 (C/D, 16 floats per lane):
@@ -117,8 +125,11 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     // would share the in-order vector-memory counter with the W2 prefetch, and waiting for
     // it would wait for the prefetched fragments too.
     __shared__ __attribute__((aligned(16))) float es[H];
-    float* red = reinterpret_cast<float*>(&h1s[0][0]);   // [kWaves][kTok][16] after GEMM2
-    static_assert(kWaves * kTok * kFeat * 4 <= 2 * kTok * HRow * 2, "reduction buffer must fit");
+    // [kWaves][kTok][16] after GEMM2, in the h1 buffer of the last chunk (the other buffer keeps
+    // the chunk a whole-output block reuses for the item's second half).
+    float* red = reinterpret_cast<float*>(&h1s[1][0]);
+    static_assert(kWaves * kTok * kFeat * 4 <= kTok * HRow * 2, "reduction buffer must fit");
+    static_assert(KCH % 2 == 0, "the last chunk of either order is consumed from buffer 1");
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     // Misses per sample (0 once a sample is done), inclusive prefix over the samples.
@@ -167,13 +178,31 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     }
     __syncthreads();
     const int nblk = d.ntok / kTok;
-    const int items = mpre[d.N] * nblk * NS;
+    const int tblocks = mpre[d.N] * nblk;            // (miss, token block) pairs
+    const int G = gridDim.x;
+    // Whole outputs (if the handle takes fresh outputs in the cache directly) unless they
+    // lengthen the launch: a block's whole item costs about 15/16 of NS half items (one
+    // gather and one h1 chunk fewer per extra half, measured ~4-6%), so they are taken when
+    // 15/16 x NS x the rounds of whole items do not exceed the rounds of half items spread
+    // over all blocks: with one item per block when more than half of the blocks get one,
+    // and always from about 7 rounds on.
+    const bool whole = d.eps_whole != nullptr && NS <= 2 &&
+                       15 * NS * ((tblocks + G - 1) / G) <= 16 * ((tblocks * NS + G - 1) / G);
+    if (d.eps_whole != nullptr && blockIdx.x == 0 && tid == 0) *d.eps_whole = whole ? 1 : 0;
     const int g = lane >> 5, l32 = lane & 31;
     const f32x16 zero16 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
                            0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     const bf16x8* w2lane = reinterpret_cast<const bf16x8*>(d.w2f) + lane;
+    // K-chunk taken at position i: natural order for even halves; odd halves start with the
+    // chunk a whole-output block still holds in buffer 0 (KCH - 2), then KCH - 1, KCH - 3, ..., 0.
+    auto korder = [&](int odd, int i) {
+        return !odd ? i : (i == 0 ? KCH - 2 : (i == 1 ? KCH - 1 : KCH - 1 - i));
+    };
+    float4 run = make_float4(0.f, 0.f, 0.f, 0.f);   // whole outputs: sum of the halves so far
     // One half (output units [512 ns, 512 ns + 512)) of the item (list entry gm, token block tb).
-    auto half = [&](int gm, int tb, int ns) {
+    // WHOLE: part of a whole-output block's item (ns > 0: the gather and the first h1 chunk of
+    // the previous half are still in LDS).
+    auto half = [&](int gm, int tb, int ns, bool whole_item) {
         int n = 0;
         while (mpre[n + 1] <= gm) ++n;               // sample of list entry gm (uniform)
         const int jm = gm - mpre[n];
@@ -182,8 +211,12 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         const int newest = d.fused_slide ? fnewest : ctrl->newest;
         const int hb0 = ns * (kNH / 32) + w * 2;   // this wave's first 32-unit block of W2^T
 
+        const int odd = ns & 1;
+        const bool reuse = whole_item && ns > 0;      // tokens, e_t and chunk KCH - 2 in LDS
         // ---- 0. gather + patchify + bf16; e_t into LDS
-        {
+        if (reuse) {
+            __syncthreads();                 // the previous half's reduction reads are done
+        } else {
             const float* xt = d.X + ((size_t)n * (d.T + 1) + min(t, newest)) * d.D;   // beyond newest: its copy
             const float* et = d.temb + (size_t)t * H;
             // Every load of the thread is issued before the first LDS store, so the block waits
@@ -249,10 +282,13 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
             h1_gelu(buf, kc, tb4, 0);
             h1_gelu(buf, kc, tb4, 2);
         };
-        h1_setup(0);
+        if (!reuse) {
+            const int k0 = korder(odd, 0);
+            h1_setup(k0);
 #pragma unroll
-        for (int tb4 = 0; tb4 < 4; ++tb4) h1_slice(h1s[0], 0, tb4);
-        __syncthreads();
+            for (int tb4 = 0; tb4 < 4; ++tb4) h1_slice(h1s[0], k0, tb4);
+            __syncthreads();
+        }
 
         f32x16 acc2[2][4];
 #pragma unroll
@@ -290,17 +326,20 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                         acc2[hb][tb4] = mfma32(A[hb][j], B[tb4 & 1][j], acc2[hb][tb4]);
             }
         };
-        // One chunk of GEMM2 (two register stages of W2^T fragments, the stream running on
-        // across chunk boundaries). MORE: chunk kc + 1 exists; its h1 slices are computed
-        // between the MFMA groups (same basic block, so the VALU work of the GELU can be
-        // interleaved with the MFMAs). A wave raises its issue priority while it feeds MFMA
-        // groups, so that the two waves of a SIMD drift out of step (one in its MFMA group
-        // while the other is in its GELU slice).
-        auto chunk = [&](int kc, auto more_c) {
+        // One chunk of GEMM2 at position i of the half's chunk order (two register stages of
+        // W2^T fragments, the stream running on across chunk boundaries); position i is in
+        // buffer i & 1. MORE: a chunk follows; its h1 slices are computed between the MFMA
+        // groups (same basic block, so the VALU work of the GELU can be interleaved with the
+        // MFMAs). A wave raises its issue priority while it feeds MFMA groups, so that the two
+        // waves of a SIMD drift out of step (one in its MFMA group while the other is in its
+        // GELU slice).
+        auto chunk = [&](int i, auto more_c) {
             constexpr bool more = decltype(more_c)::value;
-            if constexpr (more) h1_setup(kc + 1);
-            __bf16* nbuf = h1s[(kc + 1) & 1];
-            const __bf16* h1b = h1s[kc & 1] + l32 * HRow + g * 8;
+            const int kc = korder(odd, i);
+            const int kn = more ? korder(odd, i + 1) : 0;
+            if constexpr (more) h1_setup(kn);
+            __bf16* nbuf = h1s[(i + 1) & 1];
+            const __bf16* h1b = h1s[i & 1] + l32 * HRow + g * 8;
 #pragma unroll
             for (int it = 0; it < ITER; ++it) {
                 const int kb = 2 * it;
@@ -308,14 +347,14 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(1);
                 mma(A0, h1b, kb);
-                if constexpr (more) h1_slice(nbuf, kc + 1, it);
+                if constexpr (more) h1_slice(nbuf, kn, it);
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(0);
                 // Next fragments: this chunk's, or the first of the next chunk (after the
                 // last chunk an unused reload of chunk 0, kept unconditional so the wait for
                 // A1 below counts exactly these four loads as younger).
                 if (kb + 2 < KBC) load_a(A0, kc, kb + 2);
-                else load_a(A0, more ? kc + 1 : 0, 0);
+                else load_a(A0, kn, 0);
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(1);
                 mma(A1, h1b, kb + 1);
@@ -324,8 +363,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
             }
             __syncthreads();                 // chunk kc + 1 complete; chunk kc's buffer free
         };
-        load_a(A0, 0, 0);
-        for (int kc = 0; kc + 1 < KCH; ++kc) chunk(kc, std::true_type{});
+        load_a(A0, korder(odd, 0), 0);
+        for (int i = 0; i + 1 < KCH; ++i) chunk(i, std::true_type{});
         chunk(KCH - 1, std::false_type{});
 
         // ---- 3. eps^T partial = W3p GELU(h2^T) straight from the accumulators (2 GELU with W3
@@ -360,7 +399,11 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         // ---- 4. fixed-order sum over waves, unpatchify, store this half's partial output.
         // Thread = (channel c, token tl): its four features c*4 + dh*2 + dw are contiguous in
         // the reduction buffer and form two float2 pairs (dw = 0, 1) in rows 2hp and 2hp + 1.
-        float* out = d.Ep + (((size_t)ns * d.N + n) * d.P + jm) * d.D;
+        // Split outputs: this half's partial output; whole outputs: the running sum of the
+        // halves (half 0 + half 1, the order the Picard kernel adds split partials in), stored
+        // by the last half into the cache output of the miss.
+        float* out = whole_item ? d.Eh + ((size_t)n * d.T + t) * d.D
+                                : d.Ep + (((size_t)ns * d.N + n) * d.P + jm) * d.D;
         static_assert(kTok * (kFeat / 4) == NT, "one token and channel per thread");
         {
             const int tl = tid & (kTok - 1), c = tid / kTok;
@@ -373,21 +416,33 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                 sum.z += v.z;
                 sum.w += v.w;
             }
-            const int half_w = d.Wimg >> 1;
-            const int tok = tb * kTok + tl;
-            const int hp = tok / half_w, wp = tok - hp * half_w;
-            float* o = out + ((size_t)c * d.Himg + 2 * hp) * d.Wimg + 2 * wp;
-            *reinterpret_cast<float2*>(o) = make_float2(sum.x, sum.y);
-            *reinterpret_cast<float2*>(o + d.Wimg) = make_float2(sum.z, sum.w);
+            if (whole_item) {
+                run = ns == 0 ? sum : make_float4(run.x + sum.x, run.y + sum.y, run.z + sum.z, run.w + sum.w);
+                sum = run;
+            }
+            if (!whole_item || ns == NS - 1) {
+                const int half_w = d.Wimg >> 1;
+                const int tok = tb * kTok + tl;
+                const int hp = tok / half_w, wp = tok - hp * half_w;
+                float* o = out + ((size_t)c * d.Himg + 2 * hp) * d.Wimg + 2 * wp;
+                *reinterpret_cast<float2*>(o) = make_float2(sum.x, sum.y);
+                *reinterpret_cast<float2*>(o + d.Wimg) = make_float2(sum.z, sum.w);
+            }
         }
         // No barrier: the next item's gather writes xs and es only, and its barrier comes
-        // before anything overwrites the reduction buffer (the h1 buffers).
+        // before anything overwrites the reduction buffer (h1 buffer 1); a whole-output
+        // block's next half starts with one.
     };
 
-    for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        const int ns = item % NS;
-        const int rest = item / NS;
-        half(rest / nblk, rest % nblk, ns);
+    if (whole) {
+        for (int item = blockIdx.x; item < tblocks; item += G)
+            for (int ns = 0; ns < NS; ++ns) half(item / nblk, item % nblk, ns, true);
+    } else {
+        for (int item = blockIdx.x; item < tblocks * NS; item += G) {
+            const int ns = item % NS;
+            const int rest = item / NS;
+            half(rest / nblk, rest % nblk, ns, false);
+        }
     }
 }
 

@@ -3,8 +3,9 @@
 // and k_reset prepares the first window. Every kernel handles the N samples of a handle
 // at once (grid dimension y of k_reset and k_picard, the blocks of k_slide); a sample that
 // is done makes its blocks exit at once.
-//   k_picard : Eq. (6) assembly (cached output for hits, fresh for misses), Eq. (7) cache
-//              update, DDIM drift at the current latents, the Eq. (1) prefix sum over the
+//   k_picard : Eq. (6) assembly (cached output for hits, fresh for misses: in the cache
+//              already when the network launch wrote whole outputs, else the fixed-order sum
+//              of its split partials), Eq. (7) cache update, DDIM drift at the current latents, the Eq. (1) prefix sum over the
 //              window anchored at its start (blocked scan: register scan per thread, chunk
 //              carries through LDS). Per block it writes partial sums of the Eq. (2)
 //              residuals and, for the states it just updated, of the Eq. (4) deviation from
@@ -155,6 +156,9 @@ template <int TPT, bool LINEAR, int NS>
 __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     const int n = blockIdx.y;
     const Ctrl* ctrl = d.ctrl + n;
+    // The network launch wrote the fresh outputs of the misses into Eh (whole outputs) rather
+    // than split partials into Ep.
+    const bool whole = !LINEAR && d.eps_whole != nullptr && *d.eps_whole != 0;
     if (ctrl->done) return;
     const int s = ctrl->s, e = ctrl->e, W = e - s, newest = ctrl->newest;
     const int tid = threadIdx.x;
@@ -212,11 +216,13 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
         for (int h = 0; h < (NS > 1 ? NS - 1 : 1); ++h) ex[k][h] = f4_zero();
         cf[k][0] = cf[k][1] = cf[k][2] = 0.0;
         if (act) {
-            // Eq. (6): the cached output of a hit, or the network kernel's partial outputs of
-            // a miss (LINEAR: computed below from the state).
+            // Eq. (6): the cached output of a hit or of a miss with a whole fresh output, or
+            // the network kernel's partial outputs of a miss (LINEAR: computed below from the
+            // state).
             const float* ep = d.Ep + ((size_t)n * d.P + rk[k]) * D;
-            if (!(LINEAR && miss)) e0[k] = reinterpret_cast<const float4*>(miss ? ep : Eh + t * D)[c4];
-            if (!LINEAR && miss) {
+            const bool split = miss && !whole;
+            if (!(LINEAR && miss)) e0[k] = reinterpret_cast<const float4*>(split ? ep : Eh + t * D)[c4];
+            if (!LINEAR && split) {
 #pragma unroll
                 for (int h = 1; h < NS; ++h)
                     ex[k][h - 1] = reinterpret_cast<const float4*>(ep + (size_t)h * d.N * d.P * D)[c4];
@@ -247,7 +253,7 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
                 if (LINEAR) {
                     const float ct = d.lin_c[t];
                     eps = make_float4(ct * x.x, ct * x.y, ct * x.z, ct * x.w);
-                } else {
+                } else if (!whole) {
                     // Fresh output = fixed-order sum of the network kernel's partials.
 #pragma unroll
                     for (int h = 1; h < NS; ++h) {
@@ -274,8 +280,8 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     for (int k = 0; k < TPT; ++k) {
         const int j = j0 + k, t = s + j;
         if (j < W && colok && f[k]) {
-            reinterpret_cast<float4*>(Eh + t * D)[c4] = e0[k];   // Eq. (7) output
-            reinterpret_cast<float4*>(Xh + t * D)[c4] = xs[k];   // Eq. (7) input
+            if (!whole) reinterpret_cast<float4*>(Eh + t * D)[c4] = e0[k];   // Eq. (7) output
+            reinterpret_cast<float4*>(Xh + t * D)[c4] = xs[k];               // Eq. (7) input
         }
     }
     double4 pre = d4_of(anchor);

@@ -66,6 +66,8 @@ struct Dev {
     float* temb;               // [T][hidden]      e_j = temb(t_j) Wt
     float* Ep;                 // [nsplit][N][P][D] per-half network outputs of the misses
     int32_t nsplit;            // halves of the output units (partials summed by k_picard)
+    int32_t* eps_whole;        // [1] set by each network launch: 1 = it wrote whole outputs
+                               // into Eh, 0 = split partials into Ep; null = always split
     int32_t picard_blocks;
     int32_t mlp_grid;
     // Parareal sampler only (k_parareal.hip)

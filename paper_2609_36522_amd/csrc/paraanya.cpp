@@ -135,7 +135,8 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
         return fail(PA_ERR_INVALID_ARG, "window must be in [1, min(T, %d)]", PA_MAX_WINDOW);
     if (!(delta >= 0.0)) return fail(PA_ERR_INVALID_ARG, "delta must be >= 0 (got %g)", delta);
     if (!(tol >= 0.0)) return fail(PA_ERR_INVALID_ARG, "tol must be >= 0 (got %g)", tol);
-    if (flags & ~(PA_FLAG_TRACE | PA_FLAG_PROFILE | PA_FLAG_PROFILE_SOLVER)) return fail(PA_ERR_INVALID_ARG, "unknown flags");
+    if (flags & ~(PA_FLAG_TRACE | PA_FLAG_PROFILE | PA_FLAG_PROFILE_SOLVER | PA_FLAG_SPLIT_OUTPUTS))
+        return fail(PA_ERR_INVALID_ARG, "unknown flags");
     const int D = (int)Dl;
     const pa_eps_model_t* em = eps_model;
     int rc = pa::check_eps_model(em, C, Hi, Wi, T);
@@ -205,6 +206,9 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
 
     PA_HIP_BAIL(hipMemcpyAsync(d.coef, coef.data(), coef.size() * sizeof(double), hipMemcpyHostToDevice, h->stream));
     if ((rc = pa::setup_network(d, h->mem, em, tv, cus, Nz * window, h->stream))) return bail(rc);
+    // Whole network outputs written straight into the cache (unless split ones are forced).
+    if (em->kind == PA_EPS_PATCH_MLP && !(flags & PA_FLAG_SPLIT_OUTPUTS))
+        if ((rc = h->alloc(&d.eps_whole, 1, "eps_whole"))) return bail(rc);
 #undef PA_HIP_BAIL
     *out = h;
     return PA_OK;

@@ -36,6 +36,11 @@ FINAL_RTOL = 1e-4           # final latent, max-abs x RMS
 SUM_RTOL = 1e-11            # deviations/residuals: fp64 sums in different orders
 EPS_RTOL = 1e-2             # fresh network outputs, max-abs x RMS (bf16 rounding flips)
 REVISIT_THR = 0.05          # default threshold of the device's revisit counters
+# An oracle trajectory of its own (follow) stores its own fp32 states, which may differ from
+# the device's by one rounding in a few elements (the step-locked check allows that); an
+# Eq. (4) deviation, a mean of |x - x^| over D entries, then moves by (1/D) sum |diff|, a few
+# 1e-9 relative. Deviations of a followed trajectory must agree within the decision band.
+FOLLOW_DEV_RTOL = BAND
 
 
 def coefficients(T, eta=0.0):
@@ -67,8 +72,10 @@ def _in_band(v, thr) -> bool:
     return abs(v - thr) <= BAND * max(abs(thr), 1e-30)
 
 
-def _check_hits(k, dev_o, gpu, delta, log):
-    """Compare the oracle's deviations/hits (fp64) with the device's; returns the mask to use."""
+def _check_hits(k, dev_o, gpu, delta, log, rtol=SUM_RTOL):
+    """Compare the oracle's deviations/hits (fp64) with the device's; returns the mask to use.
+    ``rtol``: SUM_RTOL when both sides hold the same fp32 states (step-locked); FOLLOW_DEV_RTOL
+    when the oracle follows its own trajectory."""
     W = len(dev_o)
     assert gpu["e"] - gpu["s"] == W
     dev_g = gpu["dev"]
@@ -76,7 +83,7 @@ def _check_hits(k, dev_o, gpu, delta, log):
     ok = ~np.isnan(dev_o)
     if ok.any():
         err = np.abs(dev_g[ok] - dev_o[ok])
-        assert np.all(err <= SUM_RTOL * dev_o[ok] + 1e-300), f"sweep {k}: deviation mismatch {err.max()}"
+        assert np.all(err <= rtol * dev_o[ok] + 1e-300), f"sweep {k}: deviation mismatch {err.max()}"
     hit_o = ok & (np.nan_to_num(dev_o, nan=np.inf) < delta)
     hit_g = gpu["hit"]
     for j in np.nonzero(hit_o != hit_g)[0]:
@@ -250,7 +257,7 @@ class Run:
             e = sp.window_end(st.s, T, P)
             sp.fill_new_states(st.X, st.newest, e)
             dev_o, _ = sp.cache_test(st.X, st.Xh, st.valid, st.s, e, self.delta)
-            hit = _check_hits(k, dev_o, g, self.delta, log)
+            hit = _check_hits(k, dev_o, g, self.delta, log, rtol=FOLLOW_DEV_RTOL)
             if self.wl.model == "linear":
                 eps_fn = self.net
             else:

@@ -66,7 +66,7 @@ def _create(shape=(1, 4, 8, 8), T=10, window=4, delta=0.05, tol=1e-3, kind=B.PA_
     (dict(delta=float("nan")), "delta"),
     (dict(tol=-1.0), "tol"),
     (dict(tol=float("nan")), "tol"),
-    (dict(flags=8), "flags"),
+    (dict(flags=32), "flags"),
     (dict(flags=16), "flags"),
     (dict(null_c=True), "c is NULL"),
     (dict(kind=7), "kind"),

@@ -245,3 +245,32 @@ def test_batch_argument_checks(gpu_lib):
             with pytest.raises(B.PAError) as ei:
                 s.read_state(0, 1, bad)
             assert ei.value.code == B.PA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("wl,batch", [(W.SMALL_MLP, 1), (W.SD_MLP, 1), (W.SD_MLP, 4),
+                                      (W.Workload("mlp_4x32x32_T20_P8_H2048", (4, 32, 32), 20, 8, 0.05,
+                                                  1e-3, "patch_mlp", hidden=2048), 1)],
+                         ids=["mlp_small", "mlp_sd", "mlp_sd_batch4", "mlp_h2048"])
+def test_whole_outputs_equal_split_outputs(wl, batch, gpu_lib):
+    """A network launch writes whole outputs into the cache when that costs no extra time and
+    split partials otherwise; both give the same bits. A handle forced to split outputs on
+    every launch must end in the same trajectory, cache, counters and traces."""
+    xb = inputs.x_init_batch(wl.latent, batch).reshape(-1) if batch > 1 else inputs.x_init(wl.latent).reshape(-1)
+    x = torch.from_numpy(xb).cuda()
+    res = []
+    for split in (False, True):
+        with B.from_workload(wl, batch=batch, trace=True, split_outputs=split) as s:
+            out = s.sample(x).cpu().numpy()
+            per = [(s.stats(n), s.traces(n), s.read_state(0, None, n)) for n in range(batch)]
+        res.append((out, per))
+    (o0, p0), (o1, p1) = res
+    assert np.array_equal(o0, o1)
+    for n in range(batch):
+        (st0, tr0, S0), (st1, tr1, S1) = p0[n], p1[n]
+        assert st0 == st1, (n, st0, st1)
+        assert len(tr0) == len(tr1)
+        for a, b in zip(tr0, tr1):
+            assert a["miss"] == b["miss"] and a["c"] == b["c"]
+            assert np.array_equal(a["dev"], b["dev"], equal_nan=True) and np.array_equal(a["r"], b["r"])
+        for A, Bv in zip(S0, S1):
+            assert np.array_equal(A, Bv), n
