@@ -131,7 +131,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     static_assert(kWaves * kTok * kFeat * 4 <= kTok * HRow * 2, "reduction buffer must fit");
     static_assert(KCH % 2 == 0, "the last chunk of either order is consumed from buffer 1");
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, in a scalar register
     // Misses per sample (0 once a sample is done), inclusive prefix over the samples.
     __shared__ int mpre[PA_MAX_BATCH + 1];
     static_assert(PA_MAX_BATCH <= 64, "one wave scans the samples");
@@ -190,9 +191,11 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                        15 * NS * ((tblocks + G - 1) / G) <= 16 * ((tblocks * NS + G - 1) / G);
     if (d.eps_whole != nullptr && blockIdx.x == 0 && tid == 0) *d.eps_whole = whole ? 1 : 0;
     const int g = lane >> 5, l32 = lane & 31;
+    // W2^T as a buffer resource (out-of-range loads would return zero)
+    const __amdgpu_buffer_rsrc_t w2r = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<__bf16*>(d.w2f), (short)0, H * H * 2, 0x00020000);
     const f32x16 zero16 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
                            0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const bf16x8* w2lane = reinterpret_cast<const bf16x8*>(d.w2f) + lane;
     // K-chunk taken at position i: natural order for even halves; odd halves start with the
     // chunk a whole-output block still holds in buffer 0 (KCH - 2), then KCH - 1, KCH - 3, ..., 0.
     auto korder = [&](int odd, int i) {
@@ -297,12 +300,16 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
             for (int tb4 = 0; tb4 < 4; ++tb4) acc2[hb][tb4] = zero16;
 
         // W2^T fragments of k-block kb of chunk kc, for this wave's two 32-unit blocks.
+        // Buffer loads: the fragment's byte offset is wave-uniform (a scalar register), the
+        // lane's 16-byte slot is the only per-lane address part.
         auto load_a = [&](bf16x8 (&A)[2][2], int kc, int kb) {
-            const bf16x8* wa = w2lane + ((size_t)hb0 * KS + kc * (kKC / 16)) * 64;
+            const int sb = (hb0 * KS + kc * (kKC / 16) + 2 * kb) * 64 * 16;
 #pragma unroll
             for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
-                for (int j = 0; j < 2; ++j) A[hb][j] = wa[((size_t)hb * KS + 2 * kb + j) * 64];
+                for (int j = 0; j < 2; ++j)
+                    A[hb][j] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                        w2r, lane * 16, sb + (hb * KS + j) * 64 * 16, 0));
         };
         bf16x8 A0[2][2], A1[2][2];
         // GEMM2 MFMA group of k-block kb: 16 MFMAs over the four 32-token slices; the B
@@ -434,15 +441,11 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         // block's next half starts with one.
     };
 
-    if (whole) {
-        for (int item = blockIdx.x; item < tblocks; item += G)
-            for (int ns = 0; ns < NS; ++ns) half(item / nblk, item % nblk, ns, true);
-    } else {
-        for (int item = blockIdx.x; item < tblocks * NS; item += G) {
-            const int ns = item % NS;
-            const int rest = item / NS;
-            half(rest / nblk, rest % nblk, ns, false);
-        }
+    // One block item: both halves of a token block (whole) or one half (split).
+    const int per = whole ? NS : 1;
+    for (int item = blockIdx.x; item < tblocks * (NS / per); item += G) {
+        const int tbk = whole ? item : item / NS;
+        for (int q = 0; q < per; ++q) half(tbk / nblk, tbk % nblk, whole ? q : item % NS, whole);
     }
 }
 
