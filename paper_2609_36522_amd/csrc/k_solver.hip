@@ -130,19 +130,29 @@ hipError_t launch_reset(const Dev& d, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------- Picard
-// Block = 16 float4 columns (one DPP row) x 16 time rows, TPT slots per thread. Narrow
-// blocks give the most blocks, which this latency-bound kernel needs more than fewer partial
-// sums (measured: 64-column blocks at P = 32 take twice as long).
-constexpr int kCols = 16;
-constexpr int kRows = kThreads / kCols;
+// Block = COLS float4 columns (one DPP row of lanes) x ROWS time rows, TPT slots per thread:
+//   P <= 16: 16 x 16 x 1;  P <= 32: 16 x 16 x 2;  P <= 64: 16 x 32 x 2;  P <= 128: 16 x 64 x 2;
+//   P <= 256: 8 x 128 x 2.
+// Narrow blocks give the most blocks, which this latency-bound kernel needs more than fewer
+// partial sums (measured: 64-column blocks at P = 32 take twice as long). Longer windows take
+// more rows rather than more slots per thread: each slot holds ~30 registers, and at 8 slots
+// per thread the kernel ran at one wave per SIMD (16 slots spilled).
+struct PicardShape {
+    int cols, rows, tpt;
+};
 
-int picard_tpt(int P) {
-    int tpt = 1;
-    while (tpt * kRows < P) tpt <<= 1;
-    return tpt;
+static PicardShape picard_shape(int P) {
+    if (P <= 16) return {16, 16, 1};
+    if (P <= 32) return {16, 16, 2};
+    if (P <= 64) return {16, 32, 2};
+    if (P <= 128) return {16, 64, 2};
+    return {8, 128, 2};
 }
 
-int picard_blocks(int D) { return (D / 4 + kCols - 1) / kCols; }
+int picard_blocks(int D, int P) {
+    const int cols = picard_shape(P).cols;
+    return (D / 4 + cols - 1) / cols;
+}
 
 // LINEAR computes eps = c_t * x for the misses in place; otherwise the fresh outputs are the
 // fixed-order sum of the network kernel's partial outputs.
@@ -152,8 +162,9 @@ int picard_blocks(int D) { return (D / 4 + kCols - 1) / kCols; }
 __device__ __forceinline__ float4 f4_zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 __device__ __forceinline__ double4 d4_zero() { return make_double4(0.0, 0.0, 0.0, 0.0); }
 
-template <int TPT, bool LINEAR, int NS>
-__global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
+template <int COLS, int ROWS, int TPT, bool LINEAR, int NS>
+__global__ __launch_bounds__(COLS * ROWS) void k_picard(Dev d) {
+    constexpr int kThr = COLS * ROWS;
     const int n = blockIdx.y;
     const Ctrl* ctrl = d.ctrl + n;
     // The network launch wrote the fresh outputs of the misses into Eh (whole outputs) rather
@@ -162,9 +173,9 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     if (ctrl->done) return;
     const int s = ctrl->s, e = ctrl->e, W = e - s, newest = ctrl->newest;
     const int tid = threadIdx.x;
-    const int col = tid % kCols, row = tid / kCols;
+    const int col = tid % COLS, row = tid / COLS;
     const int n4 = d.D >> 2;
-    const int c4 = blockIdx.x * kCols + col;
+    const int c4 = blockIdx.x * COLS + col;
     const bool colok = c4 < n4;
     const int j0 = row * TPT;
     const size_t D = (size_t)d.D;
@@ -189,7 +200,7 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
     }
     __shared__ uint8_t sm[PA_MAX_WINDOW + TPT + 1];
     __shared__ uint8_t sr[PA_MAX_WINDOW + TPT];
-    static_assert(kThreads >= PA_MAX_WINDOW, "one thread per window slot");
+    static_assert(kThr >= PA_MAX_WINDOW, "one thread per window slot");
     if (tid < W) {
         sm[tid] = ctrl->slot_miss[tid];
         sr[tid] = ctrl->slot_rank[tid];
@@ -270,7 +281,7 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
 #pragma unroll
     for (int k = 1; k < TPT; ++k) dr[k] = d4_add(dr[k], dr[k - 1]);
 
-    __shared__ double4 tot[kRows][kCols];
+    __shared__ double4 tot[ROWS][COLS];
     __shared__ double rres[PA_MAX_WINDOW];
     __shared__ double rdev[PA_MAX_WINDOW];
     tot[row][col] = dr[TPT - 1];
@@ -284,8 +295,26 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
             reinterpret_cast<float4*>(Xh + t * D)[c4] = xs[k];               // Eq. (7) input
         }
     }
-    double4 pre = d4_of(anchor);
-    for (int r = 0; r < row; ++r) pre = d4_add(pre, tot[r][col]);
+    // pre = anchor + the totals of the rows above, added in row order.
+    double4 pre;
+    if constexpr (ROWS <= 16) {
+        pre = d4_of(anchor);
+        for (int r = 0; r < row; ++r) pre = d4_add(pre, tot[r][col]);
+    } else {
+        // Tall blocks: one thread per column turns the row totals into that same prefix in
+        // place (the same additions in the same order), instead of every thread re-reading
+        // up to ROWS - 1 totals.
+        if (tid < COLS) {
+            double4 acc = d4_of(anchor);
+            for (int r = 0; r < ROWS; ++r) {
+                const double4 tr = tot[r][tid];
+                tot[r][tid] = acc;
+                acc = d4_add(acc, tr);
+            }
+        }
+        __syncthreads();
+        pre = tot[row][col];
+    }
 
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
@@ -298,8 +327,8 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
             rs = sq_dev(y, xs[k + 1]);                   // Eq. (2) vs the previous iterate
             if (j + 1 < W) ds = abs_dev(y, xhn[k]);      // Eq. (4) for the next sweep
         }
-        rs = group_sum<kCols>(rs);                       // j is uniform over the 16-lane row
-        ds = group_sum<kCols>(ds);
+        rs = group_sum<COLS>(rs);                        // j is uniform over the row's lanes
+        ds = group_sum<COLS>(ds);
         if (col == 0 && j < W) {
             rres[j] = rs;
             rdev[j] = ds;
@@ -319,13 +348,15 @@ __global__ __launch_bounds__(kThreads) void k_picard(Dev d) {
 
 template <bool LINEAR, int NS>
 static hipError_t launch_picard_t(const Dev& d, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-    const dim3 grid(d.picard_blocks, d.N), block(kThreads);
-    switch (picard_tpt(d.P)) {
-        case 1: hipExtLaunchKernelGGL((k_picard<1, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 2: hipExtLaunchKernelGGL((k_picard<2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 4: hipExtLaunchKernelGGL((k_picard<4, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 8: hipExtLaunchKernelGGL((k_picard<8, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 16: hipExtLaunchKernelGGL((k_picard<16, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+    const PicardShape sh = picard_shape(d.P);
+    const dim3 grid(d.picard_blocks, d.N), block(sh.cols * sh.rows);
+    if (d.picard_blocks != picard_blocks(d.D, d.P)) return hipErrorInvalidValue;
+    switch (sh.rows * 4 + sh.tpt) {
+        case 16 * 4 + 1: hipExtLaunchKernelGGL((k_picard<16, 16, 1, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 16 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 16, 2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 32 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 32, 2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 64 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 64, 2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 128 * 4 + 2: hipExtLaunchKernelGGL((k_picard<8, 128, 2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -90,7 +90,7 @@ hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t st
 hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_temb_table(const Dev& d, const double* t_values_dev, const __bf16* wt_dev,
                              int temb_dim, hipStream_t st);
-int picard_blocks(int D);
+int picard_blocks(int D, int P);
 int mlp_supported(int hidden);
 int mlp_tokens_per_item();
 int mlp_splits(int hidden);

@@ -157,7 +157,7 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     d.N = N; d.T = T; d.P = window; d.D = D; d.C = C; d.Himg = Hi; d.Wimg = Wi;
     d.delta = delta; d.tol = tol;
     d.revisit_thr = 0.05;
-    d.picard_blocks = pa::picard_blocks(D);
+    d.picard_blocks = pa::picard_blocks(D, window);
     auto bail = [&](int code) { delete h; return code; };
 
     int dev_id = 0;
