@@ -15,6 +15,9 @@ Beside the headline line (same JSON object, extra keys):
                      sweep serves every sample's misses): samples/s, eps evals/s;
   ddpm_window64      ancestral DDPM (eta = 1, pre-drawn step noise) over T = 1000 with a
                      window of 64 on the same latent and network, delta in {0, 0.05}.
+  long_window128     the deterministic sampler over T = 1000 (the full schedule) with a window
+                     of 128 on the same latent and network, delta in {0, 0.05}: long-window
+                     prefix sums and 128-wide miss compaction; with the Picard kernel's rate.
   parareal           the Parareal-style cached sampler: 4x96x96 latent, T = 100 in 10 blocks,
                      patch-MLP H = 2048 over 2304 tokens, delta in {0, 0.05}.
   picard_beyond_cache  the solver kernels at 64 samples per handle of the same workload: one
@@ -88,7 +91,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--headline-only", action="store_true",
                     help="skip the revisit, batched, DDPM and Parareal measurements")
-    ap.add_argument("--extras", type=str, default="revisit,batched,ddpm,parareal,hbm",
+    ap.add_argument("--extras", type=str, default="revisit,batched,ddpm,long,parareal,hbm",
                     help="which extra measurements to run (comma list)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle's bounded sample")
@@ -359,6 +362,29 @@ def main():
                                    "sweeps_per_sample": r["sweeps"] / dsteps}
                           for d, r in dd.items()},
             "nfe_saved_vs_delta0": 1.0 - dd[PRIMARY_DELTA]["nfe"] / dd[0.0]["nfe"]}
+    if not args.headline_only and "long" in want:
+        # the long-window deterministic setting: T = 1000, window 128
+        wlg = workloads.LONG_MLP
+        lsteps = max(args.steps // 6, 3)
+        ll = {}
+        for d in (0.0, PRIMARY_DELTA):
+            r = run_case(wlg, d, lsteps, 1, torch, weights, solver=(d == PRIMARY_DELTA))
+            ll[d] = r
+            print(f"[bench] long T=1000 P=128 delta={d}: {1e3 * r['seconds'] / lsteps:.3f} ms/sample, "
+                  f"NFE {r['nfe'] / lsteps:.0f}, {r['sweeps'] / lsteps:.0f} sweeps", file=sys.stderr, flush=True)
+        extras["long_window128"] = {
+            "workload": wlg.name, "T": wlg.T, "window": wlg.window, "steps": lsteps,
+            "per_delta": {str(d): {"ms_per_sample": 1e3 * r["seconds"] / lsteps,
+                                   "sweeps_per_s": r["sweeps"] / r["seconds"],
+                                   "eps_evals_per_s": r["nfe"] / r["seconds"],
+                                   "nfe_per_sample": r["nfe"] / lsteps,
+                                   "hits_per_sample": r["hits"] / lsteps,
+                                   "sweeps_per_sample": r["sweeps"] / lsteps,
+                                   "eps_kernel_tflops": (r["profiled_nfe"] * fpe) / (r["eps_ms"] * 1e-3) / 1e12
+                                   if r["eps_ms"] > 0 else None}
+                          for d, r in ll.items()},
+            "nfe_saved_vs_delta0": 1.0 - ll[PRIMARY_DELTA]["nfe"] / ll[0.0]["nfe"],
+            "solver_kernels": solver_kernels(ll[PRIMARY_DELTA], wlg.D)}
     if not args.headline_only and "parareal" in want:
         # the Parareal-style cached sampler
         wp = workloads.PARAREAL_MLP
