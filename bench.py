@@ -56,11 +56,12 @@ PRIMARY_DELTA = 0.05
 
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_eps_mlp_traffic_sd_4x64x64_T100_P32_H1024.md")
 PICARD64_RECORD = os.path.join(ROOT, "profiles", "k_picard_batched64_sd_4x64x64_T100_P32_H1024.md")
+MFMA_RECORD = os.path.join(ROOT, "profiles", "k_eps_mlp_mfma_sd_4x64x64_T100_P32_H1024.md")
 
 
-def measured_traffic(record=TRAFFIC_RECORD):
-    """HBM bytes per launch of a kernel from a committed counter summary, or None when the
-    kernel sources changed since the counters were taken."""
+def counter_record(record):
+    """The machine-readable record of a committed counter summary, or None when the kernel
+    sources changed since the counters were taken."""
     import hashlib
     import re
     try:
@@ -69,11 +70,25 @@ def measured_traffic(record=TRAFFIC_RECORD):
         h = hashlib.sha256()
         for src in rec["sources"]:
             h.update(open(os.path.join(ROOT, src), "rb").read())
-        if h.hexdigest() != rec["source_sha256"]:
-            return None
-        return rec["traffic_bytes_per_launch"]
+        return rec if h.hexdigest() == rec["source_sha256"] else None
     except (OSError, AttributeError, KeyError, ValueError):
         return None
+
+
+def measured_traffic(record=TRAFFIC_RECORD):
+    """HBM bytes per launch of a kernel from a committed counter summary, or None."""
+    rec = counter_record(record)
+    return rec["traffic_bytes_per_launch"] if rec else None
+
+
+def mfma_counters():
+    """MFMA utilisation counters of the network kernel from the committed summary, or None."""
+    rec = counter_record(MFMA_RECORD)
+    if rec is None:
+        return None
+    return {k: rec[k] for k in ("mfma_busy_frac", "mfma_flop_executed_per_launch",
+                                "algorithmic_flop_per_launch", "valu_active_frac",
+                                "mfma_cycles_with_valu_coissue_frac", "clock_GHz")}
 
 
 def flops_per_eval(wl) -> float:
@@ -463,6 +478,7 @@ def main():
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
                      "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "counters": mfma_counters(),
                      "avg_launch_us": 1e3 * p["eps_ms"] / max(p["launches"], 1),
                      "flops_per_launch": p["profiled_nfe"] * fpe / max(p["launches"], 1),
                      "timing": "kernel durations from a second pass of the timed samples with "
