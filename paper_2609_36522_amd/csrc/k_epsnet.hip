@@ -142,12 +142,14 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     __shared__ int fmiss[PA_MAX_WINDOW];
     __shared__ int fnewest;
     if (d.fused_slide) {
+        static_assert(sizeof(SlideScratch) + 16 + kSlideSubDoubles * sizeof(double) <= sizeof(h1s),
+                      "slide scratch must fit");
+        SlideScratch& sc = *reinterpret_cast<SlideScratch*>(&h1s[0][0]);
+        double* sub = reinterpret_cast<double*>(&h1s[0][0] + (sizeof(SlideScratch) + 15) / 16 * 8);
         const SlidePre pre = d.pre[0];
+        slide_partials<NT>(d, 0, sub);       // its loads do not wait for the snapshot
+        __syncthreads();
         if (pre.pending) {
-            static_assert(sizeof(SlideScratch) + 16 + kSlideSubDoubles * sizeof(double) <= sizeof(h1s),
-                          "slide scratch must fit");
-            SlideScratch& sc = *reinterpret_cast<SlideScratch*>(&h1s[0][0]);
-            double* sub = reinterpret_cast<double*>(&h1s[0][0] + (sizeof(SlideScratch) + 15) / 16 * 8);
             slide_core<NT>(d, 0, pre, blockIdx.x == 0, sc, sub);
             const int m = sc.done ? 0 : sc.m;
             for (int j = tid; j < m; j += NT) fmiss[j] = sc.miss_idx[j];

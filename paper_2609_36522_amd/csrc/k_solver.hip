@@ -379,6 +379,9 @@ template <bool FROM_PRE>
 __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
     const int n = blockIdx.x;
     const Ctrl* ctrl = d.ctrl + n;
+    __shared__ SlideScratch sc;
+    __shared__ double sub[kSlideSubDoubles];
+    slide_partials<kSlideThreads>(d, n, sub);    // issued while the control block is read
     if (ctrl->done) return;
     SlidePre pre;
     if (FROM_PRE) {
@@ -387,8 +390,7 @@ __global__ __launch_bounds__(kSlideThreads) void k_slide(Dev d) {
     } else {
         pre = slide_pre_of(*ctrl);
     }
-    __shared__ SlideScratch sc;
-    __shared__ double sub[kSlideSubDoubles];
+    __syncthreads();
     slide_core<kSlideThreads>(d, n, pre, true, sc, sub);
 }
 

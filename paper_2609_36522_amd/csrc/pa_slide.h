@@ -46,42 +46,51 @@ __device__ __forceinline__ SlidePre slide_pre_of(const Ctrl& c) {
     return p;
 }
 
-// Every thread of the block calls it (it synchronizes the block). sub: kSlideSubDoubles doubles
-// of LDS. With `writer` the block publishes the result to the control block, the trace and the
-// progress word.
+// Sub-sums of the Picard kernel's partials of sample n into sub (kSlideSubDoubles doubles of
+// LDS), for all P window slots whatever the window: it reads nothing else, so a caller can
+// issue it before the pre-slide snapshot arrives. Reduction q (q < P: residual q; q >= P:
+// deviation q - P) is later the fixed-order sum of its kSlideSubs sub-sums, sub-sum u adding
+// the partials u, u + kSlideSubs, ... in order. The order does not depend on the block size,
+// so every caller (k_slide, the fused network kernel) obtains the same fp64 values bit for
+// bit; the loads of a sub-sum are independent. Slots beyond the window hold stale partials,
+// summed and never used. The caller synchronizes the block before slide_core.
 template <int NT>
-__device__ void slide_core(const Dev& d, int n, const SlidePre& pre, bool writer, SlideScratch& sc,
-                           double* sub) {
-    static_assert(NT >= 256, "block too small for the slide");
-    Ctrl* ctrl = d.ctrl + n;
-    pa_sweep_trace_t* const trace = (writer && d.trace) ? d.trace + (size_t)n * d.T : nullptr;
-    const int s = pre.s, e = pre.e, W = e - s;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nblk = d.picard_blocks;
-
-    // Residuals r of states s+1..e and deviations of states s+1..e-1 from the Picard partials:
-    // reduction q (q < W: residual q; q >= W: deviation q - W) is the fixed-order sum of its
-    // kSlideSubs sub-sums, sub-sum u adding the partials u, u + kSlideSubs, ... in order. The
-    // order does not depend on the block size, so every caller (k_slide, the fused network
-    // kernel) obtains the same fp64 values bit for bit; the loads of a sub-sum are independent.
-    const int NQ = 2 * W;
-    for (int idx = tid; idx < NQ * kSlideSubs; idx += NT) {
+__device__ void slide_partials(const Dev& d, int n, double* sub) {
+    const int tid = threadIdx.x;
+    const int nblk = d.picard_blocks, P = d.P;
+    const size_t pbase = (size_t)n * P * nblk;
+    for (int idx = tid; idx < 2 * P * kSlideSubs; idx += NT) {
         const int q = idx / kSlideSubs, u = idx - q * kSlideSubs;
-        const size_t pbase = (size_t)n * d.P * nblk;
-        const double* pr = (q < W) ? d.part_res + pbase + (size_t)q * nblk
-                                   : d.part_dev + pbase + (size_t)(q - W) * nblk;
+        const double* pr = (q < P) ? d.part_res + pbase + (size_t)q * nblk
+                                   : d.part_dev + pbase + (size_t)(q - P) * nblk;
         double acc = 0.0;
 #pragma unroll 8
         for (int b = u; b < nblk; b += kSlideSubs) acc += pr[b];
         sub[idx] = acc;
     }
-    __syncthreads();
-    for (int q = tid; q < NQ; q += NT) {
+}
+
+// Every thread of the block calls it (it synchronizes the block), after slide_partials into
+// sub and a block barrier. With `writer` the block publishes the result to the control block,
+// the trace and the progress word.
+template <int NT>
+__device__ void slide_core(const Dev& d, int n, const SlidePre& pre, bool writer, SlideScratch& sc,
+                           const double* sub) {
+    static_assert(NT >= 256, "block too small for the slide");
+    Ctrl* ctrl = d.ctrl + n;
+    pa_sweep_trace_t* const trace = (writer && d.trace) ? d.trace + (size_t)n * d.T : nullptr;
+    const int s = pre.s, e = pre.e, W = e - s;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int P = d.P;
+
+    // Residuals r of states s+1..e and deviations of states s+1..e-1.
+    for (int i = tid; i < 2 * W; i += NT) {
+        const int q = i < W ? i : P + (i - W);
         double v = 0.0;
 #pragma unroll
         for (int u = 0; u < kSlideSubs; ++u) v += sub[q * kSlideSubs + u];
-        if (q < W) sc.r[q] = v / (double)d.D;
-        else sc.dv[q - W] = v / (double)d.D;
+        if (i < W) sc.r[i] = v / (double)d.D;
+        else sc.dv[i - W] = v / (double)d.D;
     }
     __syncthreads();
 
