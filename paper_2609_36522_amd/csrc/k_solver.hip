@@ -198,6 +198,31 @@ __global__ __launch_bounds__(COLS * ROWS) void k_picard(Dev d) {
         const int j = j0 + k;
         xs[k] = (j <= W && colok) ? reinterpret_cast<const float4*>(X + min(s + j, newest) * D)[c4] : f4_zero();
     }
+    // Loads that do not depend on the miss flags, issued before the flags are staged: the
+    // coefficients, the step noise and, when the network launch wrote whole outputs, each
+    // slot's row of Eh.
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {
+        const int j = j0 + k, t = s + j;
+        const bool act = j < W && colok;
+        e0[k] = f4_zero();
+        zt[k] = f4_zero();
+        xhn[k] = f4_zero();
+#pragma unroll
+        for (int h = 0; h < (NS > 1 ? NS - 1 : 1); ++h) ex[k][h] = f4_zero();
+        cf[k][0] = cf[k][1] = cf[k][2] = 0.0;
+        if (act) {
+            // Eq. (6) with whole outputs: the cache row holds the output of a hit and the
+            // fresh output of a miss alike.
+            if (whole) e0[k] = reinterpret_cast<const float4*>(Eh + t * D)[c4];
+            cf[k][0] = d.coef[3 * t];
+            cf[k][1] = d.coef[3 * t + 1];
+            if (noise) {
+                cf[k][2] = d.coef[3 * t + 2];
+                zt[k] = reinterpret_cast<const float4*>(noise + t * D)[c4];
+            }
+        }
+    }
     __shared__ uint8_t sm[PA_MAX_WINDOW + TPT + 1];
     __shared__ uint8_t sr[PA_MAX_WINDOW + TPT];
     static_assert(kThr >= PA_MAX_WINDOW, "one thread per window slot");
@@ -214,35 +239,21 @@ __global__ __launch_bounds__(COLS * ROWS) void k_picard(Dev d) {
 #pragma unroll
     for (int k = 0; k < TPT; ++k) rk[k] = (j0 + k < W) ? sr[j0 + k] : 0;
 
-    // ---- every other load of the thread, issued before any store.
+    // ---- the loads that depend on the flags, issued before any store.
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
         const int j = j0 + k, t = s + j;
         const bool act = j < W && colok;
         const bool miss = f[k] != 0;
-        e0[k] = f4_zero();
-        zt[k] = f4_zero();
-        xhn[k] = f4_zero();
-#pragma unroll
-        for (int h = 0; h < (NS > 1 ? NS - 1 : 1); ++h) ex[k][h] = f4_zero();
-        cf[k][0] = cf[k][1] = cf[k][2] = 0.0;
-        if (act) {
-            // Eq. (6): the cached output of a hit or of a miss with a whole fresh output, or
-            // the network kernel's partial outputs of a miss (LINEAR: computed below from the
-            // state).
+        if (act && !whole) {
+            // Eq. (6): the cached output of a hit, or the network kernel's split partial
+            // outputs of a miss (LINEAR: computed below from the state).
             const float* ep = d.Ep + ((size_t)n * d.P + rk[k]) * D;
-            const bool split = miss && !whole;
-            if (!(LINEAR && miss)) e0[k] = reinterpret_cast<const float4*>(split ? ep : Eh + t * D)[c4];
-            if (!LINEAR && split) {
+            if (!(LINEAR && miss)) e0[k] = reinterpret_cast<const float4*>(miss ? ep : Eh + t * D)[c4];
+            if (!LINEAR && miss) {
 #pragma unroll
                 for (int h = 1; h < NS; ++h)
                     ex[k][h - 1] = reinterpret_cast<const float4*>(ep + (size_t)h * d.N * d.P * D)[c4];
-            }
-            cf[k][0] = d.coef[3 * t];
-            cf[k][1] = d.coef[3 * t + 1];
-            if (noise) {
-                cf[k][2] = d.coef[3 * t + 2];
-                zt[k] = reinterpret_cast<const float4*>(noise + t * D)[c4];
             }
         }
         // Cache entry the updated state s + 1 + j is tested against in the next sweep: the
