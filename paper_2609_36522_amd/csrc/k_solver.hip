@@ -162,8 +162,10 @@ int picard_blocks(int D, int P) {
 __device__ __forceinline__ float4 f4_zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 __device__ __forceinline__ double4 d4_zero() { return make_double4(0.0, 0.0, 0.0, 0.0); }
 
-template <int COLS, int ROWS, int TPT, bool LINEAR, int NS>
-__global__ __launch_bounds__(COLS * ROWS) void k_picard(Dev d) {
+// MINB: minimum blocks per CU the compiler must fit (1, or 5 for the 256-thread shape of
+// batched handles: at most 96 registers, five waves per SIMD).
+template <int COLS, int ROWS, int TPT, bool LINEAR, int NS, int MINB>
+__global__ __launch_bounds__(COLS * ROWS, MINB) void k_picard(Dev d) {
     constexpr int kThr = COLS * ROWS;
     const int n = blockIdx.y;
     const Ctrl* ctrl = d.ctrl + n;
@@ -362,12 +364,24 @@ static hipError_t launch_picard_t(const Dev& d, hipStream_t st, hipEvent_t e0, h
     const PicardShape sh = picard_shape(d.P);
     const dim3 grid(d.picard_blocks, d.N), block(sh.cols * sh.rows);
     if (d.picard_blocks != picard_blocks(d.D, d.P)) return hipErrorInvalidValue;
+    // Batched handles stream from HBM with many blocks per CU: five waves per SIMD instead of
+    // four took 93 -> 86 us per launch at 64 samples (one sample: within 2% either way, and the
+    // four-wave build is kept there). With four partial outputs the register cap would spill.
+    const bool occ = d.N >= 8;
     switch (sh.rows * 4 + sh.tpt) {
-        case 16 * 4 + 1: hipExtLaunchKernelGGL((k_picard<16, 16, 1, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 16 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 16, 2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 32 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 32, 2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 64 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 64, 2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 128 * 4 + 2: hipExtLaunchKernelGGL((k_picard<8, 128, 2, LINEAR, NS>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 16 * 4 + 1: hipExtLaunchKernelGGL((k_picard<16, 16, 1, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 16 * 4 + 2:
+            if constexpr (NS <= 2) {
+                if (occ) {
+                    hipExtLaunchKernelGGL((k_picard<16, 16, 2, LINEAR, NS, 5>), grid, block, 0, st, e0, e1, 0, d);
+                    break;
+                }
+            }
+            hipExtLaunchKernelGGL((k_picard<16, 16, 2, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d);
+            break;
+        case 32 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 32, 2, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 64 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 64, 2, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 128 * 4 + 2: hipExtLaunchKernelGGL((k_picard<8, 128, 2, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
