@@ -231,9 +231,10 @@ def run_case(wl, delta, steps, warmup, torch, weights, *, batch=1, eta=0.0, solv
 
 
 def measured_ceilings(torch, gemm_m):
-    """Ceilings measured on this GPU beside the vendor peaks: a plain 1 GiB device copy
-    (HBM), and hipBLASLt bf16 GEMMs run as a library through torch.matmul, at the network's
-    GEMM2 shape for one sweep's misses ([gemm_m x 1024] x [1024 x 1024]) and at 8192^3."""
+    """Ceilings measured on this GPU beside the vendor peaks: HBM streams of 1 GiB arrays
+    through torch (a copy, a fill that only writes, and z = x + y, two reads per write), and
+    hipBLASLt bf16 GEMMs run as a library through torch.matmul, at the network's GEMM2 shape
+    for one sweep's misses ([gemm_m x 1024] x [1024 x 1024]) and at 8192^3."""
     def timed(fn, reps):
         fn()
         torch.cuda.synchronize()
@@ -250,8 +251,13 @@ def measured_ceilings(torch, gemm_m):
     dst = torch.empty_like(src)
     t = timed(lambda: dst.copy_(src), 10)
     copy_gbs = 2 * n * 4 / t / 1e9
-    del src, dst
-    out = {"copy_1GiB_GBps": copy_gbs}
+    t = timed(lambda: dst.fill_(2.0), 10)
+    fill_gbs = n * 4 / t / 1e9
+    third = torch.empty_like(src)
+    t = timed(lambda: torch.add(src, dst, out=third), 10)
+    add_gbs = 3 * n * 4 / t / 1e9
+    del src, dst, third
+    out = {"copy_1GiB_GBps": copy_gbs, "fill_1GiB_GBps": fill_gbs, "add_1GiB_GBps": add_gbs}
     for name, (m, k, nn) in {"gemm2_shape": (gemm_m, 1024, 1024), "square_8192": (8192, 8192, 8192)}.items():
         A = torch.randn(m, k, device="cuda", dtype=torch.bfloat16)
         Bm = torch.randn(k, nn, device="cuda", dtype=torch.bfloat16)
@@ -490,10 +496,13 @@ def main():
         line["measured_ceilings"] = ceil
         line["roofline"]["frac_vs_measured_square_gemm"] = achieved / ceil["bf16_square_8192_TFLOPs"]
         line["roofline"]["frac_vs_measured_gemm2_shape"] = achieved / ceil["bf16_gemm2_shape_TFLOPs"]
-        for key in ("solver_kernels",):
-            pk = line[key]["k_picard"]
+        pks = [line["solver_kernels"]["k_picard"]]
+        if "picard_beyond_cache" in line:
+            pks.append(line["picard_beyond_cache"]["solver_kernels"]["k_picard"])
+        for pk in pks:
             if pk["achieved"]:
                 pk["frac_vs_measured_copy"] = pk["achieved"] / ceil["copy_1GiB_GBps"]
+                pk["frac_vs_measured_add"] = pk["achieved"] / ceil["add_1GiB_GBps"]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, PRIMARY_DELTA, args.cpu_seconds)
         if not args.headline_only:
