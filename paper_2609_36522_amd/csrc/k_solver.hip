@@ -162,9 +162,10 @@ int picard_blocks(int D, int P) {
 __device__ __forceinline__ float4 f4_zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 __device__ __forceinline__ double4 d4_zero() { return make_double4(0.0, 0.0, 0.0, 0.0); }
 
-// MINB: minimum blocks per CU the compiler must fit (1, or 5 for the 256-thread shape of
-// batched handles: at most 96 registers, five waves per SIMD).
-template <int COLS, int ROWS, int TPT, bool LINEAR, int NS, int MINB>
+// MINB: minimum blocks per CU the compiler must fit (1, or 6 (5 with step noise or one
+// partial output) for the 256-thread shape of batched handles: at most 76 (96) registers). NOISE: the step adds the
+// pre-drawn noise term (stochastic sampler).
+template <int COLS, int ROWS, int TPT, bool LINEAR, int NS, int MINB, bool NOISE>
 __global__ __launch_bounds__(COLS * ROWS, MINB) void k_picard(Dev d) {
     constexpr int kThr = COLS * ROWS;
     const int n = blockIdx.y;
@@ -184,7 +185,7 @@ __global__ __launch_bounds__(COLS * ROWS, MINB) void k_picard(Dev d) {
     float* X = d.X + (size_t)n * (d.T + 1) * D;
     float* Xh = d.Xh + (size_t)n * d.T * D;
     float* Eh = d.Eh + (size_t)n * d.T * D;
-    const float* noise = d.noise ? d.noise + (size_t)n * d.T * D : nullptr;
+    const float* noise = NOISE ? d.noise + (size_t)n * d.T * D : nullptr;
 
     // ---- the states (independent of the miss list) first; meanwhile the block stages the
     // per-slot miss flags and ranks in LDS, so that the address of every other load is known
@@ -219,7 +220,7 @@ __global__ __launch_bounds__(COLS * ROWS, MINB) void k_picard(Dev d) {
             if (whole) e0[k] = reinterpret_cast<const float4*>(Eh + t * D)[c4];
             cf[k][0] = d.coef[3 * t];
             cf[k][1] = d.coef[3 * t + 1];
-            if (noise) {
+            if (NOISE) {
                 cf[k][2] = d.coef[3 * t + 2];
                 zt[k] = reinterpret_cast<const float4*>(noise + t * D)[c4];
             }
@@ -287,7 +288,7 @@ __global__ __launch_bounds__(COLS * ROWS, MINB) void k_picard(Dev d) {
                 }
             }
             dr[k] = drift(cf[k][0], x, cf[k][1], eps);
-            if (noise) dr[k] = add_noise(dr[k], cf[k][2], zt[k]);
+            if (NOISE) dr[k] = add_noise(dr[k], cf[k][2], zt[k]);
             e0[k] = eps;
         }
     }
@@ -359,42 +360,49 @@ __global__ __launch_bounds__(COLS * ROWS, MINB) void k_picard(Dev d) {
     if (d.fused_slide && blockIdx.x == 0 && tid == 0) d.pre[n] = slide_pre_of(*ctrl);
 }
 
-template <bool LINEAR, int NS>
+template <bool LINEAR, int NS, bool NOISE>
 static hipError_t launch_picard_t(const Dev& d, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const PicardShape sh = picard_shape(d.P);
     const dim3 grid(d.picard_blocks, d.N), block(sh.cols * sh.rows);
     if (d.picard_blocks != picard_blocks(d.D, d.P)) return hipErrorInvalidValue;
-    // Batched handles stream from HBM with many blocks per CU: five waves per SIMD instead of
-    // four took 93 -> 86 us per launch at 64 samples (one sample: within 2% either way, and the
-    // four-wave build is kept there). With four partial outputs the register cap would spill.
+    // Batched handles stream from HBM with many blocks per CU: a build capped at 76 registers
+    // (six waves per SIMD; 96 and five with step noise or one partial output, whose registers
+    // would otherwise spill) instead of four waves (one sample: within 2% either way, and the four-wave build is kept
+    // there). With four partial outputs the register cap would spill.
     const bool occ = d.N >= 8;
     switch (sh.rows * 4 + sh.tpt) {
-        case 16 * 4 + 1: hipExtLaunchKernelGGL((k_picard<16, 16, 1, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 16 * 4 + 1: hipExtLaunchKernelGGL((k_picard<16, 16, 1, LINEAR, NS, 1, NOISE>), grid, block, 0, st, e0, e1, 0, d); break;
         case 16 * 4 + 2:
             if constexpr (NS <= 2) {
                 if (occ) {
-                    hipExtLaunchKernelGGL((k_picard<16, 16, 2, LINEAR, NS, 5>), grid, block, 0, st, e0, e1, 0, d);
+                    constexpr int kMinb = (NOISE || NS == 1) ? 5 : 6;
+                    hipExtLaunchKernelGGL((k_picard<16, 16, 2, LINEAR, NS, kMinb, NOISE>), grid, block, 0, st, e0, e1, 0, d);
                     break;
                 }
             }
-            hipExtLaunchKernelGGL((k_picard<16, 16, 2, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d);
+            hipExtLaunchKernelGGL((k_picard<16, 16, 2, LINEAR, NS, 1, NOISE>), grid, block, 0, st, e0, e1, 0, d);
             break;
-        case 32 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 32, 2, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 64 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 64, 2, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d); break;
-        case 128 * 4 + 2: hipExtLaunchKernelGGL((k_picard<8, 128, 2, LINEAR, NS, 1>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 32 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 32, 2, LINEAR, NS, 1, NOISE>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 64 * 4 + 2: hipExtLaunchKernelGGL((k_picard<16, 64, 2, LINEAR, NS, 1, NOISE>), grid, block, 0, st, e0, e1, 0, d); break;
+        case 128 * 4 + 2: hipExtLaunchKernelGGL((k_picard<8, 128, 2, LINEAR, NS, 1, NOISE>), grid, block, 0, st, e0, e1, 0, d); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t e0, hipEvent_t e1) {
-    if (linear) return launch_picard_t<true, 1>(d, st, e0, e1);
+template <bool NOISE>
+static hipError_t launch_picard_n(const Dev& d, hipStream_t st, int linear, hipEvent_t e0, hipEvent_t e1) {
+    if (linear) return launch_picard_t<true, 1, NOISE>(d, st, e0, e1);
     switch (d.nsplit) {
-        case 1: return launch_picard_t<false, 1>(d, st, e0, e1);
-        case 2: return launch_picard_t<false, 2>(d, st, e0, e1);
-        case 4: return launch_picard_t<false, 4>(d, st, e0, e1);
+        case 1: return launch_picard_t<false, 1, NOISE>(d, st, e0, e1);
+        case 2: return launch_picard_t<false, 2, NOISE>(d, st, e0, e1);
+        case 4: return launch_picard_t<false, 4, NOISE>(d, st, e0, e1);
         default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t e0, hipEvent_t e1) {
+    return d.noise ? launch_picard_n<true>(d, st, linear, e0, e1) : launch_picard_n<false>(d, st, linear, e0, e1);
 }
 
 // ---------------------------------------------------------------------------- slide
