@@ -51,7 +51,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kTok = 128;               // tokens per work item
+constexpr int kTokMax = 128;            // tokens per work item (64 for single-latent launches)
 constexpr int kNH = 512;                // GEMM2 output units per work item
 constexpr int kKC = 256;                // h1 units per LDS buffer (K-chunk); two buffers
 constexpr int kWaves = 8;               // wave w owns output units [64w, 64w + 64) of the item
@@ -93,8 +93,11 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 struct TokPos {
     int tl, f, idx;
 };
+template <int kTok>
 __device__ __forceinline__ TokPos tok_pos(int e, int tb, int Himg, int Wimg) {
-    const int dw = e & 1, tl = (e >> 1) & (kTok - 1), dh = (e >> 8) & 1, c = e >> 9;
+    constexpr int kLog = kTok == 128 ? 7 : 6;
+    static_assert(kTok == (1 << kLog), "64 or 128 tokens per item");
+    const int dw = e & 1, tl = (e >> 1) & (kTok - 1), dh = (e >> (kLog + 1)) & 1, c = e >> (kLog + 2);
     const int half_w = Wimg >> 1;
     const int tok = tb * kTok + tl;
     const int hp = tok / half_w, wp = tok - hp * half_w;
@@ -107,9 +110,13 @@ __device__ __forceinline__ TokPos tok_pos(int e, int tb, int Himg, int Wimg) {
 
 }  // namespace
 
-template <int H>
+// TOK: tokens per work item, 128, or 64 for launches of a single latent (twice the work items,
+// each half as long, where 128-token items would leave most CUs idle).
+template <int H, int TOK>
 __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     constexpr int NT = kWaves * 64;
+    constexpr int kTok = TOK;
+    constexpr int TB4 = kTok / 32;       // 32-token slices per item
     constexpr int NS = H / kNH;          // halves of the output units (work items per tokens)
     constexpr int KCH = H / kKC;         // K-chunks of h1
     constexpr int HRow = kKC + 8;        // padded LDS row of h1 (bf16)
@@ -232,13 +239,13 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
             float xv[kPer];
             float4 ev[kEs];
 #pragma unroll
-            for (int k = 0; k < kPer; ++k) xv[k] = xt[tok_pos(tid + k * NT, tb, d.Himg, d.Wimg).idx];
+            for (int k = 0; k < kPer; ++k) xv[k] = xt[tok_pos<kTok>(tid + k * NT, tb, d.Himg, d.Wimg).idx];
 #pragma unroll
             for (int k = 0; k < kEs; ++k)
                 if (tid + k * NT < H / 4) ev[k] = reinterpret_cast<const float4*>(et)[tid + k * NT];
 #pragma unroll
             for (int k = 0; k < kPer; ++k) {
-                const TokPos p = tok_pos(tid + k * NT, tb, d.Himg, d.Wimg);
+                const TokPos p = tok_pos<kTok>(tid + k * NT, tb, d.Himg, d.Wimg);
                 xs[p.tl * kXRow + p.f] = (__bf16)xv[k];
             }
 #pragma unroll
@@ -291,15 +298,15 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
             const int k0 = korder(odd, 0);
             h1_setup(k0);
 #pragma unroll
-            for (int tb4 = 0; tb4 < 4; ++tb4) h1_slice(h1s[0], k0, tb4);
+            for (int tb4 = 0; tb4 < TB4; ++tb4) h1_slice(h1s[0], k0, tb4);
             __syncthreads();
         }
 
-        f32x16 acc2[2][4];
+        f32x16 acc2[2][TB4];
 #pragma unroll
         for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
-            for (int tb4 = 0; tb4 < 4; ++tb4) acc2[hb][tb4] = zero16;
+            for (int tb4 = 0; tb4 < TB4; ++tb4) acc2[hb][tb4] = zero16;
 
         // W2^T fragments of k-block kb of chunk kc, for this wave's two 32-unit blocks.
         // Buffer loads: the fragment's byte offset is wave-uniform (a scalar register), the
@@ -321,8 +328,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
 #pragma unroll
             for (int j = 0; j < 2; ++j) B[0][j] = *reinterpret_cast<const bf16x8*>(h1b + kb * 32 + j * 16);
 #pragma unroll
-            for (int tb4 = 0; tb4 < 4; ++tb4) {
-                if (tb4 + 1 < 4) {
+            for (int tb4 = 0; tb4 < TB4; ++tb4) {
+                if (tb4 + 1 < TB4) {
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
                         B[(tb4 + 1) & 1][j] = *reinterpret_cast<const bf16x8*>(
@@ -356,7 +363,9 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(1);
                 mma(A0, h1b, kb);
-                if constexpr (more) h1_slice(nbuf, kn, it);
+                if constexpr (more) {
+                    if (it < TB4) h1_slice(nbuf, kn, it);   // one 32-token slice per iteration
+                }
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_setprio(0);
                 // Next fragments: this chunk's, or the first of the next chunk (after the
@@ -378,7 +387,9 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
 
         // ---- 3. eps^T partial = W3p GELU(h2^T) straight from the accumulators (2 GELU with W3
         // stored halved)
-        f32x16 acc3[4] = {zero16, zero16, zero16, zero16};
+        f32x16 acc3[TB4];
+#pragma unroll
+        for (int tb4 = 0; tb4 < TB4; ++tb4) acc3[tb4] = zero16;
 #pragma unroll
         for (int hb = 0; hb < 2; ++hb) {
 #pragma unroll
@@ -386,7 +397,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
                 const bf16x8 a3 = *reinterpret_cast<const bf16x8*>(
                     d.w3p + (((size_t)(hb0 + hb) * 2 + jj) * 64 + lane) * 8);
 #pragma unroll
-                for (int tb4 = 0; tb4 < 4; ++tb4) {
+                for (int tb4 = 0; tb4 < TB4; ++tb4) {
                     bf16x8 b3;
 #pragma unroll
                     for (int i = 0; i < 8; ++i) b3[i] = (__bf16)gelu2_erf(acc2[hb][tb4][jj * 8 + i]);
@@ -396,7 +407,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         }
         // valid rows of acc3: regs 0..7 -> feature (r/4)*8 + g*4 + r%4, token tb4*32 + l32
 #pragma unroll
-        for (int tb4 = 0; tb4 < 4; ++tb4) {
+        for (int tb4 = 0; tb4 < TB4; ++tb4) {
             float* dst = red + ((size_t)w * kTok + tb4 * 32 + l32) * kFeat;
             *reinterpret_cast<float4*>(dst + g * 4) =
                 make_float4(acc3[tb4][0], acc3[tb4][1], acc3[tb4][2], acc3[tb4][3]);
@@ -413,8 +424,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
         // by the last half into the cache output of the miss.
         float* out = whole_item ? d.Eh + ((size_t)n * d.T + t) * d.D
                                 : d.Ep + (((size_t)ns * d.N + n) * d.P + jm) * d.D;
-        static_assert(kTok * (kFeat / 4) == NT, "one token and channel per thread");
-        {
+        static_assert(kTok * (kFeat / 4) <= NT, "one token and channel per thread");
+        if (tid < kTok * (kFeat / 4)) {
             const int tl = tid & (kTok - 1), c = tid / kTok;
             float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
@@ -453,23 +464,21 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
 
 int mlp_supported(int hidden) { return hidden == 512 || hidden == 1024 || hidden == 2048; }
 
-int mlp_tokens_per_item() { return kTok; }
+int mlp_tokens_per_item() { return kTokMax; }
 
 int mlp_splits(int hidden) { return hidden / kNH; }
 
 int mlp_grid_size(int device_cus) { return device_cus > 0 ? device_cus : 256; }
 
-hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
-    switch (d.hidden) {
-        case 512:
-            hipExtLaunchKernelGGL(k_eps_mlp<512>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, start, stop, 0, d);
-            break;
-        case 1024:
-            hipExtLaunchKernelGGL(k_eps_mlp<1024>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, start, stop, 0, d);
-            break;
-        case 2048:
-            hipExtLaunchKernelGGL(k_eps_mlp<2048>, dim3(d.mlp_grid), dim3(kWaves * 64), 0, st, start, stop, 0, d);
-            break;
+hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop, int single) {
+    const dim3 grid(d.mlp_grid), block(kWaves * 64);
+    switch (d.hidden * 2 + (single ? 1 : 0)) {
+        case 512 * 2: hipExtLaunchKernelGGL((k_eps_mlp<512, 128>), grid, block, 0, st, start, stop, 0, d); break;
+        case 512 * 2 + 1: hipExtLaunchKernelGGL((k_eps_mlp<512, 64>), grid, block, 0, st, start, stop, 0, d); break;
+        case 1024 * 2: hipExtLaunchKernelGGL((k_eps_mlp<1024, 128>), grid, block, 0, st, start, stop, 0, d); break;
+        case 1024 * 2 + 1: hipExtLaunchKernelGGL((k_eps_mlp<1024, 64>), grid, block, 0, st, start, stop, 0, d); break;
+        case 2048 * 2: hipExtLaunchKernelGGL((k_eps_mlp<2048, 128>), grid, block, 0, st, start, stop, 0, d); break;
+        case 2048 * 2 + 1: hipExtLaunchKernelGGL((k_eps_mlp<2048, 64>), grid, block, 0, st, start, stop, 0, d); break;
         default:
             return hipErrorInvalidValue;
     }

@@ -87,7 +87,8 @@ hipError_t launch_slide_pending(const Dev& d, hipStream_t st);
 // Largest fp64 partial-sum volume per sample the network kernel reduces redundantly per block.
 constexpr size_t kFusedSlideMaxBytes = 256 * 1024;
 hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t start, hipEvent_t stop);
-hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop);
+// single: the launch evaluates at most one latent (64-token work items).
+hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop, int single = 0);
 hipError_t launch_temb_table(const Dev& d, const double* t_values_dev, const __bf16* wt_dev,
                              int temb_dim, hipStream_t st);
 int picard_blocks(int D, int P);

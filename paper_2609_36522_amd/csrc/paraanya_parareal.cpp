@@ -64,7 +64,9 @@ struct paraanya_parareal {
                 const int rc = timer.pair(0, &e0, &e1);
                 if (rc) return rc;
             }
-            PA_HIP(pa::launch_eps_mlp(d, stream, e0, e1));
+            // A coarse request evaluates one latent: 64-token work items spread it over twice
+            // as many CUs.
+            PA_HIP(pa::launch_eps_mlp(d, stream, e0, e1, step_kernel == pa::PRK_COARSE ? 1 : 0));
         }
         PA_HIP(pa::launch_pr(d, a, step_kernel, stream));
         return PA_OK;
