@@ -274,3 +274,24 @@ def test_whole_outputs_equal_split_outputs(wl, batch, gpu_lib):
             assert np.array_equal(a["dev"], b["dev"], equal_nan=True) and np.array_equal(a["r"], b["r"])
         for A, Bv in zip(S0, S1):
             assert np.array_equal(A, Bv), n
+
+
+@pytest.mark.parametrize("wl,batch", [(W.TINY_LINEAR, 3), (W.SMALL_MLP, 1)], ids=["linear_batch3", "mlp"])
+def test_sample_output_alignment(wl, batch, gpu_lib):
+    """Buffers at any 4-byte offset and an aliased x_init == x_out give the same final
+    latents, bit for bit, and the same counters."""
+    xs = inputs.x_init_batch(wl.latent, batch).reshape(-1) if batch > 1 else inputs.x_init(wl.latent).reshape(-1)
+    n = xs.size
+    big = torch.zeros(n + 4, device="cuda")
+    with B.from_workload(wl, batch=batch) as s:
+        x = torch.from_numpy(xs).cuda()
+        ref = s.sample(x).cpu().numpy()
+        st = s.stats()
+        big[1:n + 1] = x                      # 4-byte offset: not 16-byte aligned
+        out_big = torch.zeros(n + 4, device="cuda")
+        s.sample(big[1:n + 1], out_big[3:n + 3])
+        assert np.array_equal(out_big[3:n + 3].cpu().numpy(), ref)
+        assert s.stats() == st
+        y = x.clone()
+        s.sample(y, y)                        # in place
+        assert np.array_equal(y.cpu().numpy(), ref)
