@@ -480,7 +480,7 @@ def main():
                       for d, r in per_delta.items()},
         "solver_kernels": solver_kernels(
             run_case(wl, PRIMARY_DELTA, 10, 1, torch, weights, solver=True), wl.D),
-        "roofline": {"bound": "mfma", "kernel": "k_eps_mlp<1024>",
+        "roofline": {"bound": "mfma", "kernel": "k_eps_mlp<1024, 128>",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
                      "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
