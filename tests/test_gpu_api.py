@@ -175,13 +175,16 @@ def test_stochastic_handle_needs_noise(gpu_lib):
         assert ei.value.code == B.PA_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("wl,eta", [(W.TINY_LINEAR, 0.0), (W.SMALL_MLP, 0.0), (W.SD_MLP, 0.0),
-                                    (W.TINY_LINEAR, 1.0), (W.SMALL_MLP, 1.0)],
-                         ids=["linear", "mlp_small", "mlp_sd", "linear_ddpm", "mlp_small_ddpm"])
-def test_batch_equals_independent_samples(wl, eta, gpu_lib):
+@pytest.mark.parametrize("wl,eta,N", [(W.TINY_LINEAR, 0.0, 4), (W.SMALL_MLP, 0.0, 4), (W.SD_MLP, 0.0, 4),
+                                      (W.TINY_LINEAR, 1.0, 4), (W.SMALL_MLP, 1.0, 4),
+                                      (W.SD_MLP, 0.0, 8), (W.SMALL_MLP, 1.0, 8), (W.TINY_LINEAR, 0.0, 8)],
+                         ids=["linear", "mlp_small", "mlp_sd", "linear_ddpm", "mlp_small_ddpm",
+                              "mlp_sd_batch8", "mlp_small_ddpm_batch8", "linear_batch8"])
+def test_batch_equals_independent_samples(wl, eta, N, gpu_lib):
     """A handle with N samples gives each sample exactly what a single-sample handle gives
-    it: the same final latent bit for bit, counters and sweep traces."""
-    N = 4
+    it: the same final latent bit for bit, counters and sweep traces. Handles of eight or more
+    samples run the Picard kernel builds capped for occupancy (deterministic, stochastic and
+    linear-network builds)."""
     xb = inputs.x_init_batch(wl.latent, N).reshape(N, -1)
     Z = inputs.step_noise(N, wl.T, wl.D) if eta > 0 else None
     with B.from_workload(wl, batch=N, eta=eta, trace=True) as s:
