@@ -54,6 +54,8 @@ extern "C" {
 
 #define PA_MAX_WINDOW 256        /* largest window P */
 #define PA_MAX_BATCH  64         /* largest number of samples N per handle */
+#define PA_MAX_STEPS  (1 << 20)  /* largest number of sampling steps T (keeps T + 1 and every
+                                    row count of the trajectory within int) */
 
 /* ------------------------------------------------------------------ schedule */
 #define PA_SCHED_SCALED_LINEAR 0
@@ -173,14 +175,14 @@ typedef struct {
 
 /* ------------------------------------------------------------------ entry points */
 
-/* Create a sampler. latent_shape = {N, C, H, W} with 1 <= N <= PA_MAX_BATCH samples; T >= 1 sampling steps;
+/* Create a sampler. latent_shape = {N, C, H, W} with 1 <= N <= PA_MAX_BATCH samples; T in [1, PA_MAX_STEPS] sampling steps;
  * window P in [1, min(T, PA_MAX_WINDOW)]; delta >= 0 the cache tolerance of Eq. (5)
  * (strict '<'; 0 disables hits; +inf allowed); tol >= 0 the tau of Eq. (2) (mean
  * square, '<='). Both thresholds are compared against fp64 sums: states and network
  * outputs are stored in fp32, and the drift, the Picard sum, the deviations and the
  * residuals are computed in fp64 from them, then rounded once on store. stream is a hipStream_t (NULL = the null stream). On success *out
  * holds the handle; on failure *out = NULL and nothing is left allocated.
- * Errors: INVALID_ARG (N outside [1, PA_MAX_BATCH], C*H*W % 4 != 0, T < 1, window outside
+ * Errors: INVALID_ARG (N outside [1, PA_MAX_BATCH], C*H*W % 4 != 0, T outside [1, PA_MAX_STEPS], window outside
  * range, delta or tol negative/NaN, eta outside [0, 1], bad schedule or model fields),
  * UNSUPPORTED (model shape not built), OOM, HIP. */
 PA_API int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_t* schedule,
@@ -300,8 +302,8 @@ typedef struct {
     double  dev;          /* Eq. (4) (fp64 sum); NaN without a cache entry */
 } pa_request_trace_t;
 
-/* Create a Parareal sampler. latent_shape = {1, C, H, W}; blocks in [1, PA_PR_MAX_BLOCKS]
- * dividing T; delta, tol as for paraanya_create; flags: PA_FLAG_TRACE (request records,
+/* Create a Parareal sampler. latent_shape = {1, C, H, W}; T in [1, PA_MAX_STEPS]; blocks in
+ * [1, PA_PR_MAX_BLOCKS] dividing T; delta, tol as for paraanya_create; flags: PA_FLAG_TRACE (request records,
  * fresh outputs and boundary residuals), PA_FLAG_PROFILE (network launch timings).
  * Errors: INVALID_ARG, UNSUPPORTED (eta != 0, model shape not built), OOM, HIP. */
 PA_API int paraanya_parareal_create(const int32_t latent_shape[4], int32_t T,

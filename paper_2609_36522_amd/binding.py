@@ -23,6 +23,7 @@ PA_ERR_NONFINITE = -5
 PA_ERR_UNSUPPORTED = -6
 PA_MAX_WINDOW = 256
 PA_MAX_BATCH = 64
+PA_MAX_STEPS = 1 << 20
 PA_PR_MAX_BLOCKS = 64
 
 PA_SCHED_SCALED_LINEAR = 0

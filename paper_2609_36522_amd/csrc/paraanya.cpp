@@ -130,7 +130,7 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     const long long Dl = (long long)C * Hi * Wi;
     if (Dl % 4 != 0) return fail(PA_ERR_INVALID_ARG, "C*H*W must be a multiple of 4");
     if (Dl > (1ll << 30)) return fail(PA_ERR_INVALID_ARG, "latent too large");
-    if (T < 1) return fail(PA_ERR_INVALID_ARG, "T must be >= 1");
+    if (T < 1 || T > PA_MAX_STEPS) return fail(PA_ERR_INVALID_ARG, "T must be in [1, %d] (got %d)", PA_MAX_STEPS, T);
     if (window < 1 || window > T || window > PA_MAX_WINDOW)
         return fail(PA_ERR_INVALID_ARG, "window must be in [1, min(T, %d)]", PA_MAX_WINDOW);
     if (!(delta >= 0.0)) return fail(PA_ERR_INVALID_ARG, "delta must be >= 0 (got %g)", delta);

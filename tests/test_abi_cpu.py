@@ -59,6 +59,7 @@ def _create(shape=(1, 4, 8, 8), T=10, window=4, delta=0.05, tol=1e-3, kind=B.PA_
     (dict(eta=float("nan")), "eta"),
     (dict(shape=(1, 3, 3, 3)), "multiple of 4"),
     (dict(T=0, window=1), "T must"),
+    (dict(T=B.PA_MAX_STEPS + 1, window=4), "T must"),
     (dict(window=0), "window"),
     (dict(window=11), "window"),
     (dict(T=300, window=257), "window"),
@@ -172,6 +173,7 @@ def _pr_create(shape=(1, 4, 8, 8), T=20, blocks=4, delta=0.05, tol=1e-3, eta=0.0
     (dict(shape=(2, 4, 8, 8)), B.PA_ERR_INVALID_ARG, "batch"),
     (dict(blocks=3), B.PA_ERR_INVALID_ARG, "blocks"),
     (dict(blocks=0), B.PA_ERR_INVALID_ARG, "blocks"),
+    (dict(T=B.PA_MAX_STEPS + 1, blocks=1), B.PA_ERR_INVALID_ARG, "T must"),
     (dict(T=130, blocks=65), B.PA_ERR_INVALID_ARG, "blocks"),
     (dict(delta=-1.0), B.PA_ERR_INVALID_ARG, "delta"),
     (dict(tol=float("nan")), B.PA_ERR_INVALID_ARG, "tol"),
