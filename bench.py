@@ -108,8 +108,8 @@ def parse():
                     help="skip the revisit, batched, DDPM and Parareal measurements")
     ap.add_argument("--extras", type=str, default="revisit,batched,ddpm,long,parareal,hbm",
                     help="which extra measurements to run (comma list)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="budget of the oracle's bounded sample")
+    ap.add_argument("--cpu-seconds", type=float, default=6.0,
+                    help="budget of each of the oracle's two bounded samples (all threads, one)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
     return ap.parse_args()
@@ -123,9 +123,12 @@ def timed_samples(sampler, x, steps, warmup, torch, profiled):
     if profiled:
         sampler.kernel_times()                      # restart the kernel timers
     sweeps = nfe = hits = revisits = below = 0
+    per_sample = []
     t0 = time.perf_counter()
     for _ in range(steps):
-        sampler.sample(x, out)
+        ts = time.perf_counter()
+        sampler.sample(x, out)                      # returns after the stream is synchronized
+        per_sample.append(time.perf_counter() - ts)
         st = sampler.stats()                        # host mirror of the last synchronization
         sweeps += st["sweeps"]
         nfe += st["nfe"]
@@ -134,8 +137,11 @@ def timed_samples(sampler, x, steps, warmup, torch, profiled):
         below += st["revisits_below"]
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    per_sample.sort()
     r = {"seconds": dt, "sweeps": sweeps, "nfe": nfe, "hits": hits, "revisits": revisits,
-         "revisits_below": below, "out": out}
+         "revisits_below": below, "out": out,
+         "median_sample_s": per_sample[len(per_sample) // 2] if len(per_sample) % 2 else
+         0.5 * (per_sample[len(per_sample) // 2 - 1] + per_sample[len(per_sample) // 2])}
     if profiled:
         kt = sampler.kernel_times()                 # every launch of the timed samples
         r.update({"eps_ms": kt["eps_ms_total"], "launches": kt["launches"],
@@ -200,6 +206,22 @@ def solver_kernels(r, D):
                         if r["slide_ms"] > 0 else
                         {"fused": "computed at the start of the next network kernel (one "
                                   "patch-MLP sample): no launch of its own"})}
+
+
+def sweep_breakdown(p, rs, steps):
+    """Where a sweep's stream time goes at the headline workload, in microseconds per sweep:
+    total = wall time of a sample (plain launches) / its sweeps; network = event-timed
+    duration of the network launches of a sample / sweeps; picard = event-timed duration of
+    the Picard launches (a run whose handle also times them) / sweeps; rest = total - network
+    - picard: launch gaps, the window slide's own launch when it has one, and the host's
+    enqueue and final copy."""
+    sweeps = p["sweeps"] / steps
+    total = 1e6 * p["seconds"] / steps / sweeps
+    net = 1e3 * p["eps_ms"] / steps / sweeps
+    pic = 1e3 * rs["picard_ms"] / rs["profiled_sweeps"] if rs["profiled_sweeps"] else 0.0
+    sld = 1e3 * rs["slide_ms"] / rs["profiled_sweeps"] if rs["profiled_sweeps"] else 0.0
+    return {"total": total, "network": net, "picard": pic, "slide": sld,
+            "rest": total - net - pic - sld, "sweeps_per_sample": sweeps}
 
 
 def run_case(wl, delta, steps, warmup, torch, weights, *, batch=1, eta=0.0, solver=False):
@@ -292,7 +314,20 @@ def cpu_baseline(wl, delta, budget_s):
     return {"value": st.sweeps / dt, "unit": "sweeps/s", "cores": int(threads), "kind": "oracle",
             "sample": f"first {st.sweeps} sweeps (NFE {st.nfe}, {dt:.1f} s) of the delta={delta} "
                       f"sample, float64 NumPy oracle",
-            "eps_evals_per_s": st.nfe / dt}
+            "eps_evals_per_s": st.nfe / dt, "cpu_model": cpu_model(),
+            "os_cpu_count": os.cpu_count()}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():
@@ -442,6 +477,7 @@ def main():
 
     p = per_delta[PRIMARY_DELTA]
     d0 = per_delta.get(0.0)
+    rs = run_case(wl, PRIMARY_DELTA, 10, 1, torch, weights, solver=True)
     sweeps_per_s = p["sweeps"] / p["seconds"]
     eps_per_s = p["nfe"] / p["seconds"]
     achieved = (p["profiled_nfe"] * fpe) / (p["eps_ms"] * 1e-3) / 1e12 if p["eps_ms"] > 0 else 0.0
@@ -453,6 +489,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": 1e3 * p["seconds"] / args.steps,
+        "ms_per_sample_mean": 1e3 * p["seconds"] / args.steps,
+        "ms_per_sample_median": 1e3 * p["median_sample_s"],
+        "sweeps_per_s_median": (p["sweeps"] / args.steps) / p["median_sample_s"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -471,6 +510,7 @@ def main():
         "per_delta": {str(d): {"sweeps_per_s": r["sweeps"] / r["seconds"],
                                "eps_evals_per_s": r["nfe"] / r["seconds"],
                                "ms_per_sample": 1e3 * r["seconds"] / args.steps,
+                               "ms_per_sample_median": 1e3 * r["median_sample_s"],
                                "nfe_per_sample": r["nfe"] / args.steps,
                                "hits_per_sample": r["hits"] / args.steps,
                                "sweeps_per_sample": r["sweeps"] / args.steps,
@@ -478,8 +518,8 @@ def main():
                                "eps_kernel_tflops": ((r["profiled_nfe"] * fpe) / (r["eps_ms"] * 1e-3) / 1e12
                                                      if r["eps_ms"] > 0 else None)}
                       for d, r in per_delta.items()},
-        "solver_kernels": solver_kernels(
-            run_case(wl, PRIMARY_DELTA, 10, 1, torch, weights, solver=True), wl.D),
+        "solver_kernels": solver_kernels(rs, wl.D),
+        "sweep_breakdown_us": sweep_breakdown(p, rs, args.steps),
         "roofline": {"bound": "mfma", "kernel": "k_eps_mlp<1024, 128>",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),

@@ -28,11 +28,14 @@ F32 = np.float32
 
 # --------------------------------------------------------------------------- bf16
 def bf16_round(x) -> np.ndarray:
-    """Round fp32 values to the nearest bf16 value (ties to even); returns fp32."""
+    """Round fp32 values to the nearest bf16 value (ties to even); returns fp32.
+
+    Adding 0x7FFF plus the lowest kept bit to the fp32 bit pattern and clearing the low 16
+    bits rounds to nearest even. In 32-bit arithmetic only NaN patterns can wrap around;
+    they are passed through unchanged."""
     a = np.ascontiguousarray(x, dtype=F32)
-    u = a.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = (((u + 0x7FFF + lsb) >> 16) << 16).astype(np.uint32).view(F32)
+    u = a.view(np.uint32)
+    r = ((u + (((u >> 16) & np.uint32(1)) + np.uint32(0x7FFF))) & np.uint32(0xFFFF0000)).view(F32)
     return np.where(np.isnan(a), a, r).reshape(a.shape)
 
 

@@ -74,6 +74,7 @@ struct KernelTimer {
         for (hipEvent_t e : pool) (void)hipEventDestroy(e);
     }
     int pair(int k, hipEvent_t* e0, hipEvent_t* e1);
+    size_t pending() const { return kind.size(); }   // pairs handed out since the last drain
     int drain();                       // the stream must be synchronized
     void clear();
 };

@@ -66,11 +66,19 @@ struct paraanya {
         return false;
     }
 
-    // Start/stop events of one timed launch of kernel kind k, or nulls when untimed.
+    // Start/stop events of one timed launch of kernel kind k, or nulls when untimed. Samples
+    // drain the pool when they end; a handle driven sweep by sweep drains it (after waiting
+    // for the stream) once kMaxPendingPairs launches are pending.
+    static constexpr size_t kMaxPendingPairs = 4096;
     int timed(int k, hipEvent_t* e0, hipEvent_t* e1) {
         *e0 = *e1 = nullptr;
         if (!(flags & PA_FLAG_PROFILE)) return PA_OK;
         if (k > 0 && !(flags & PA_FLAG_PROFILE_SOLVER)) return PA_OK;
+        if (timer.pending() >= kMaxPendingPairs) {
+            PA_HIP(hipStreamSynchronize(stream));
+            const int rc = timer.drain();
+            if (rc) return rc;
+        }
         return timer.pair(k, e0, e1);
     }
 
@@ -331,6 +339,10 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
     h->ctrl_fresh = false;
     if ((rc = h->read_ctrl())) return rc;
     for (int n = 0; n < N; ++n) h->timed_latents += h->ctrl_host[n].nfe;
+    // The stream is idle (read_ctrl synchronized it): fold this sample's event pairs into the
+    // running totals, so the pool stays at one sample's launches.
+    if (h->flags & PA_FLAG_PROFILE)
+        if ((rc = h->timer.drain())) return rc;
     if (h->any_nonfinite()) return fail(PA_ERR_NONFINITE, "non-finite residual during sampling");
     return PA_OK;
 }

@@ -232,6 +232,10 @@ int paraanya_parareal_sample(paraanya_parareal_t* h, const float* x_init, float*
     st.done = pc.done;
     st.nonfinite = pc.nonfinite;
     h->timed_latents += st.nfe;
+    // The stream is idle: fold this sample's event pairs into the running totals, so the
+    // pool stays at one sample's launches however many samples run between reads.
+    if (h->flags & PA_FLAG_PROFILE)
+        if ((rc = h->timer.drain())) return rc;
     if (pc.nonfinite) return fail(PA_ERR_NONFINITE, "non-finite boundary residual");
     return PA_OK;
 }

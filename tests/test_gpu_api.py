@@ -127,9 +127,14 @@ def test_profile_counts_launches(gpu_lib):
         s.sample(_x(wl))
         kt = s.kernel_times()
         st = s.stats()
+        # several samples between reads: each sample folds its launches into the totals
+        for _ in range(3):
+            s.sample(_x(wl))
+        kt3 = s.kernel_times()
     # sample() may enqueue a sweep or two past done; those network launches exit at once.
     assert kt["launches"] >= st["sweeps"] and kt["eps_latents"] == st["nfe"]
     assert kt["eps_ms_total"] > 0
+    assert kt3["launches"] >= 3 * st["sweeps"] and kt3["eps_latents"] == 3 * st["nfe"]
     assert kt["solver_launches"] == 0 and kt["picard_ms_total"] == 0.0
     with B.from_workload(wl, profile_solver=True) as s:
         s.sample(_x(wl))
@@ -298,3 +303,41 @@ def test_sample_output_alignment(wl, batch, gpu_lib):
         y = x.clone()
         s.sample(y, y)                        # in place
         assert np.array_equal(y.cpu().numpy(), ref)
+
+
+def _create_raw(latent, T, window, c):
+    """paraanya_create through ctypes, *out preset to a non-NULL value; returns (rc, handle)."""
+    import ctypes as C
+    lib = B.load_library()
+    keep = []
+    sc, em_ = B._schedule_and_model(keep, None, 0.0, "linear", c, None, 0)
+    shape = (C.c_int32 * 4)(1, *latent)
+    h = C.c_void_p(0x1234)
+    rc = lib.paraanya_create(shape, int(T), C.byref(sc), int(window), 0.05, 1e-3, C.byref(em_),
+                             C.c_void_p(torch.cuda.current_stream().cuda_stream), 0, C.byref(h))
+    return rc, h
+
+
+def test_create_out_of_memory_fails_cleanly(gpu_lib):
+    """Device buffers beyond the device's memory: create fails with PA_ERR_OOM before any
+    sweep, sets *out to NULL and frees whatever it had allocated; the next valid create and
+    sample work. Two sizes: the first buffer (the trajectory) alone is too large, and the
+    trajectory and cached inputs fit but the cached outputs do not."""
+    torch.cuda.synchronize()
+    free0, total = torch.cuda.mem_get_info()
+    lat = (4, 8192, 8192)                       # 1 GiB per state
+    row = 4 * 8192 * 8192 * 4
+    for T in (1000, int(0.4 * free0 // row)):
+        assert 1 <= T <= 1000 and (T == 1000 or 2 * (T + 1) * row < free0)
+        c = np.full(T, 0.9, np.float32)
+        print(f"[oom] T={T}: {T * row / 2**30:.1f} GiB per [T][D] buffer, {free0 / 2**30:.1f} GiB free", flush=True)
+        rc, h = _create_raw(lat, T, 1, c)
+        assert rc == B.PA_ERR_OOM, (rc, B.status_str(rc))
+        assert h.value is None
+        torch.cuda.synchronize()
+        free1, _ = torch.cuda.mem_get_info()
+        assert free1 >= free0 - (64 << 20), f"{(free0 - free1) / 2**20:.0f} MiB not returned"
+    wl = W.TINY_LINEAR
+    with B.from_workload(wl) as s:
+        out = s.sample(_x(wl)).cpu().numpy()
+        assert s.stats()["done"] and np.isfinite(out).all()

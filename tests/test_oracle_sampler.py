@@ -115,12 +115,61 @@ def _decisions(records):
 
 
 def _band_ok(a_rec, b_rec, delta, tau, rel=1e-9):
-    """True if every differing decision lies within rel of its threshold."""
+    """True if two decision traces differ only through a decision taken within rel of its
+    threshold (Eq. (5) for hits, Eq. (2) for the converged count).
+
+    Up to the first such flip every window, hit mask, miss list, converged count and slide
+    must be equal. In the sweep of the flip, hit masks may differ only in slots whose
+    deviation lies within the band of delta on both sides, each miss list must be the one
+    its own mask gives, and converged counts may differ only if the residual that ends the
+    shorter count lies within the band of tau on both sides. After the flip the two runs
+    hold different states, so later sweeps are not comparable and are not compared. A
+    difference with no such flip (a miss list, a count or a slide that differs while the
+    masks agree) fails."""
+    near = lambda v, thr: abs(v - thr) <= rel * max(abs(thr), 1e-300)
     for ra, rb in zip(a_rec, b_rec):
-        for da, ha, hb in zip(ra["dev"], ra["hit"], rb["hit"]):
-            if bool(ha) != bool(hb) and not abs(da - delta) <= rel * max(delta, 1e-300):
+        if (ra["s"], ra["e"]) != (rb["s"], rb["e"]):
+            return False
+        W = ra["e"] - ra["s"]
+        for r in (ra, rb):
+            if list(r["miss"]) != [r["s"] + j for j in range(W) if not r["hit"][j]]:
                 return False
-    return True
+            if r["s_next"] != r["s"] + 1 + r["c"]:
+                return False
+        flipped = False
+        for j in range(W):
+            if bool(ra["hit"][j]) != bool(rb["hit"][j]):
+                if not (near(ra["dev"][j], delta) and near(rb["dev"][j], delta)):
+                    return False
+                flipped = True
+        if flipped:
+            return True
+        if ra["c"] != rb["c"]:
+            j = min(ra["c"], rb["c"])
+            return j < W - 1 and near(ra["r"][j], tau) and near(rb["r"][j], tau)
+    return False
+
+
+def test_band_ok_rejects_differences_outside_the_band():
+    """The pin's fallback accepts an in-band flip and nothing else."""
+    base = {"s": 0, "e": 3, "hit": [False, True, False], "dev": [np.nan, 0.01, 0.2],
+            "miss": [0, 2], "r": [1e-4, 2e-3, 5e-3], "c": 1, "s_next": 2}
+    same = dict(base)
+    assert not _band_ok([base], [same], 0.05, 1e-3)                  # no flip: not explained
+    miss = dict(base, miss=[0, 1])                                   # same mask, other list
+    assert not _band_ok([base], [miss], 0.05, 1e-3)
+    count = dict(base, c=0, s_next=1)                                # count differs, r far
+    assert not _band_ok([base], [count], 0.05, 1e-3)
+    near_tau = dict(base, r=[1e-3, 2e-3, 5e-3])
+    assert _band_ok([near_tau], [dict(near_tau, c=0, s_next=1)], 0.05, 1e-3)
+    hit_far = dict(base, hit=[False, False, False], miss=[0, 1, 2])  # flip at dev 0.01
+    assert not _band_ok([base], [hit_far], 0.05, 1e-3)
+    near_d = dict(base, dev=[np.nan, 0.05, 0.2])
+    assert _band_ok([near_d], [dict(near_d, hit=[False, False, False], miss=[0, 1, 2])], 0.05, 1e-3)
+    first = dict(base, hit=[True, True, False], miss=[2])            # a first entry "hit"
+    assert not _band_ok([base], [first], 0.05, 1e-3)
+    slide = dict(base, s_next=3)                                     # slide not s + 1 + c
+    assert not _band_ok([base], [slide], 0.05, 1e-3)
 
 
 GRID = [(T, P, d, tau) for T in range(1, 13) for P in range(1, T + 1)
