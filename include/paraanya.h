@@ -262,6 +262,31 @@ PA_API int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out);
 /* Free every resource of the handle (synchronizes its stream first). NULL-safe. */
 PA_API void paraanya_destroy(paraanya_t* h);
 
+/* ------------------------------------------------------------------ allocation-free sampling
+ * For callers that cannot allocate: code that must not call hipMalloc, hipHostMalloc or
+ * hipFree (tight serving loops, harnesses that forbid allocation). One complete sample, the
+ * same bit for bit as paraanya_create (flags 0) + paraanya_sample + paraanya_stats +
+ * paraanya_destroy with the same arguments, but every device buffer of the sampler
+ * (trajectory, cache, partial sums, control blocks, progress words, network tables) is carved
+ * from a static device workspace of PA_NOALLOC_WORKSPACE_BYTES that the library holds on each
+ * device it runs on until the process ends, and the host side uses the stack only. No device,
+ * pinned or host heap memory is allocated (an error message may allocate its text).
+ * Arguments as for paraanya_create, plus: x_init, x_out device N x D fp32 (may alias);
+ * stats (host, may be NULL) receives the counters as paraanya_stats reports them. Limits:
+ * T <= PA_NOALLOC_MAX_STEPS, deterministic step (schedule eta = 0), and the request's
+ * buffers must fit the workspace (e.g. one 4x64x64 latent, T = 100, window 32, patch-MLP
+ * hidden 1024 takes about 28 MiB); otherwise INVALID_ARG (UNSUPPORTED for eta != 0) before
+ * anything is enqueued. Returns after x_out is written (the stream is synchronized). Calls on
+ * one device share its workspace and are serialized by a lock inside the library; every call
+ * rebuilds the workspace's contents (the previous call's are overwritten), and calls that
+ * overlapped on one device without that lock would race. Other errors as paraanya_sample. */
+#define PA_NOALLOC_WORKSPACE_BYTES (64u << 20)
+#define PA_NOALLOC_MAX_STEPS 1024
+PA_API int paraanya_sample_noalloc(const int32_t latent_shape[4], int32_t T,
+                                   const pa_schedule_t* schedule, int32_t window, double delta,
+                                   double tol, const pa_eps_model_t* eps_model, void* stream,
+                                   const float* x_init, float* x_out, pa_stats_t* stats);
+
 /* ------------------------------------------------------------------ Parareal sampler
  * The Parareal-based sampler family of Sec. 2.1 (coarse solver initializing, fine solvers
  * refining; SRDS) with the Sec. 2.2 cache on every network evaluation, coarse or fine. The

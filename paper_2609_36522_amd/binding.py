@@ -44,7 +44,9 @@ EXPORTED = ("paraanya_create", "paraanya_reset", "paraanya_sweep", "paraanya_sam
             "paraanya_parareal_create", "paraanya_parareal_sample", "paraanya_parareal_stats",
             "paraanya_parareal_trace", "paraanya_parareal_residuals",
             "paraanya_parareal_read_boundaries", "paraanya_parareal_kernel_times",
-            "paraanya_parareal_destroy")
+            "paraanya_parareal_destroy", "paraanya_sample_noalloc")
+PA_NOALLOC_WORKSPACE_BYTES = 64 << 20
+PA_NOALLOC_MAX_STEPS = 1024
 
 
 class Schedule(C.Structure):
@@ -147,6 +149,8 @@ def load_library(path: str = LIB_PATH):
     lib.paraanya_parareal_kernel_times.argtypes = [P, C.POINTER(KTimes)]
     lib.paraanya_parareal_destroy.argtypes = [P]
     lib.paraanya_parareal_destroy.restype = None
+    lib.paraanya_sample_noalloc.argtypes = [C.POINTER(C.c_int32), I32, C.POINTER(Schedule), I32, F64, F64,
+                                            C.POINTER(EpsModel), V, P, P, C.POINTER(Stats)]
     lib.paraanya_last_error.restype = C.c_char_p
     lib.paraanya_status_str.argtypes = [C.c_int]
     lib.paraanya_status_str.restype = C.c_char_p
@@ -351,6 +355,44 @@ def from_workload(wl, delta=None, *, seed_weights=None, **kw) -> "Sampler":
     return Sampler(wl.latent, wl.T, wl.window, d, wl.tol, "patch_mlp", weights=w,
                    hidden=wl.hidden, **kw)
 
+
+
+def sample_noalloc(latent, T, window, delta, tol, model, x_init, x_out=None, *, c=None, weights=None,
+                   hidden=0, schedule=None, stream=None, batch=1):
+    """paraanya_sample_noalloc: one sample with every device buffer in the library's static
+    workspace (no allocation by the library). ``x_init`` (and ``x_out``, allocated here by torch
+    when None) are contiguous fp32 CUDA tensors of batch x D values. Returns (x_out, stats)."""
+    import torch
+    lib = load_library()
+    latent = tuple(int(v) for v in latent)
+    D = int(np.prod(latent))
+    st = stream if stream is not None else torch.cuda.current_stream()
+    for t in (x_init,) + (() if x_out is None else (x_out,)):
+        if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.float32 and t.is_contiguous()
+                and t.numel() == batch * D):
+            raise ValueError(f"expected a contiguous fp32 CUDA tensor of {batch * D} elements")
+    if x_out is None:
+        x_out = torch.empty_like(x_init)
+    keep = []
+    sc, em = _schedule_and_model(keep, schedule, 0.0, model, c, weights, hidden)
+    shape = (C.c_int32 * 4)(int(batch), *latent)
+    out = Stats()
+    _check(lib.paraanya_sample_noalloc(shape, int(T), C.byref(sc), int(window), float(delta), float(tol),
+                                       C.byref(em), C.c_void_p(st.cuda_stream), C.c_void_p(x_init.data_ptr()),
+                                       C.c_void_p(x_out.data_ptr()), C.byref(out)))
+    return x_out, out.as_dict()
+
+
+def sample_noalloc_workload(wl, x_init, x_out=None, delta=None, *, seed_weights=None, **kw):
+    """sample_noalloc for a :class:`~paper_2609_36522_amd.workloads.Workload` with its seeded inputs."""
+    from . import inputs
+    d = wl.delta if delta is None else delta
+    if wl.model == "linear":
+        return sample_noalloc(wl.latent, wl.T, wl.window, d, wl.tol, "linear", x_init, x_out,
+                              c=inputs.linear_coefficients(wl.T), **kw)
+    w = inputs.mlp_weights(wl.hidden, temb_dim=wl.temb_dim) if seed_weights is None else seed_weights
+    return sample_noalloc(wl.latent, wl.T, wl.window, d, wl.tol, "patch_mlp", x_init, x_out, weights=w,
+                          hidden=wl.hidden, **kw)
 
 
 class Parareal:

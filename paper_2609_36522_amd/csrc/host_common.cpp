@@ -28,9 +28,9 @@ int hip_fail(hipError_t e, const char* what) {
     return fail(PA_ERR_HIP, "%s failed: %s", what, hipGetErrorString(e));
 }
 
-int build_schedule(const pa_schedule_t* sc, int T, std::vector<double>& ab, std::vector<double>& tv) {
-    ab.assign(T + 1, 0.0);
-    tv.assign(T, 0.0);
+int build_schedule(const pa_schedule_t* sc, int T, double* ab, double* tv) {
+    for (int i = 0; i <= T; ++i) ab[i] = 0.0;
+    for (int j = 0; j < T; ++j) tv[j] = 0.0;
     if (sc->kind == PA_SCHED_SCALED_LINEAR) {
         const int N = sc->train_steps;
         if (!(N >= 2) || !(T <= N)) return fail(PA_ERR_INVALID_ARG, "schedule: need 2 <= train_steps and T <= train_steps");
@@ -38,19 +38,21 @@ int build_schedule(const pa_schedule_t* sc, int T, std::vector<double>& ab, std:
             return fail(PA_ERR_INVALID_ARG, "schedule: betas must lie in (0, 1)");
         if (sc->spacing != PA_SPACING_TRAILING) return fail(PA_ERR_UNSUPPORTED, "schedule: only trailing spacing is built");
         if (sc->final_alpha_one != 1) return fail(PA_ERR_UNSUPPORTED, "schedule: only final_alpha_one = 1 is built");
-        std::vector<double> abar(N);
-        double prod = 1.0;
-        const double r0 = sqrt(sc->beta_start), r1 = sqrt(sc->beta_end);
-        for (int j = 0; j < N; ++j) {
-            const double r = r0 + j * (r1 - r0) / (N - 1);
-            prod *= 1.0 - r * r;
-            abar[j] = prod;
-        }
         for (int j = 0; j < T; ++j) {
             const long t = lrint(nearbyint((double)N - j * (double)N / T)) - 1;  // ties to even
             if (t < 0 || t >= N) return fail(PA_ERR_INVALID_ARG, "schedule: timestep out of range");
             tv[j] = (double)t;
-            ab[j] = abar[t];
+        }
+        // alpha_bar(t) = prod_{k <= t} (1 - beta_k), taken at the timesteps t_j as the running
+        // product passes them (t_j strictly decreases with j: consecutive steps are at least
+        // one train step apart).
+        double prod = 1.0;
+        const double r0 = sqrt(sc->beta_start), r1 = sqrt(sc->beta_end);
+        int j = T - 1;
+        for (int k = 0; k < N && j >= 0; ++k) {
+            const double r = r0 + k * (r1 - r0) / (N - 1);
+            prod *= 1.0 - r * r;
+            while (j >= 0 && tv[j] == (double)k) ab[j--] = prod;
         }
         ab[T] = 1.0;
     } else if (sc->kind == PA_SCHED_EXPLICIT) {
@@ -68,10 +70,15 @@ int build_schedule(const pa_schedule_t* sc, int T, std::vector<double>& ab, std:
     return PA_OK;
 }
 
-std::vector<double> step_coefficients(const std::vector<double>& ab, int T, double eta) {
+int build_schedule(const pa_schedule_t* sc, int T, std::vector<double>& ab, std::vector<double>& tv) {
+    ab.assign(T + 1, 0.0);
+    tv.assign(T, 0.0);
+    return build_schedule(sc, T, ab.data(), tv.data());
+}
+
+void step_coefficients(const double* ab, int T, double eta, double* coef) {
     // One-step increment d_i = alpha_i x_i + b_i eps_i + sigma_i z_i of the generalized DDIM
     // step with eta (eta = 0: DDIM; eta = 1: ancestral DDPM).
-    std::vector<double> coef(3 * (size_t)T);
     for (int i = 0; i < T; ++i) {
         const double a = sqrt(ab[i + 1] / ab[i]);
         const double sig = eta * sqrt((1.0 - ab[i + 1]) / (1.0 - ab[i])) * sqrt(1.0 - ab[i] / ab[i + 1]);
@@ -79,6 +86,11 @@ std::vector<double> step_coefficients(const std::vector<double>& ab, int T, doub
         coef[3 * i + 1] = sqrt(1.0 - ab[i + 1] - sig * sig) - a * sqrt(1.0 - ab[i]);
         coef[3 * i + 2] = sig;
     }
+}
+
+std::vector<double> step_coefficients(const std::vector<double>& ab, int T, double eta) {
+    std::vector<double> coef(3 * (size_t)T);
+    step_coefficients(ab.data(), T, eta, coef.data());
     return coef;
 }
 
@@ -138,21 +150,7 @@ void KernelTimer::clear() {
     }
 }
 
-// Half of a bf16 value (bit pattern in, bit pattern out), rounded to nearest even. Exact for
-// every normal value (the exponent drops by one); only a subnormal with its lowest mantissa bit
-// set, or the smallest normal's odd neighbours, round.
-static uint16_t bf16_half(uint16_t b) {
-    uint32_t u = (uint32_t)b << 16;
-    float f;
-    memcpy(&f, &u, 4);
-    f *= 0.5f;
-    memcpy(&u, &f, 4);
-    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)(u >> 16);   // inf / NaN
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
-
-int setup_network(Dev& d, DevMem& mem, const pa_eps_model_t* em, const std::vector<double>& tv,
+int setup_network(Dev& d, DevMem& mem, const pa_eps_model_t* em, const double* tv,
                   int cus, size_t ep_rows, hipStream_t st) {
     const int T = d.T;
     const size_t Dz = (size_t)d.D;
@@ -167,50 +165,32 @@ int setup_network(Dev& d, DevMem& mem, const pa_eps_model_t* em, const std::vect
     d.hidden = Hd;
     d.ntok = (d.Himg / 2) * (d.Wimg / 2);
     d.mlp_grid = mlp_grid_size(cus);
-    // Device layouts: W1^T [H][16]; W2^T as MFMA A fragments, fragment (b, ks) = lanes
-    // l = 0..63 x 8 values W2[16 ks + 8 (l/32) + i][32 b + l%32]; W3 fragments permuted
-    // to the GEMM2 accumulator layout (see k_epsnet.hip). W2 and W3 are stored halved: the
-    // kernels feed them twice the GELU outputs, so every product is the unscaled one.
-    std::vector<uint16_t> w1t((size_t)Hd * 16), w2f((size_t)Hd * Hd), w3p((size_t)Hd * 32);
-    for (int f = 0; f < 16; ++f)
-        for (int n = 0; n < Hd; ++n) w1t[(size_t)n * 16 + f] = em->w1[(size_t)f * Hd + n];
-    const int KS = Hd / 16;
-    for (int b = 0; b < Hd / 32; ++b)
-        for (int ks = 0; ks < KS; ++ks)
-            for (int lane = 0; lane < 64; ++lane)
-                for (int i = 0; i < 8; ++i) {
-                    const int n = b * 32 + (lane & 31), k = ks * 16 + (lane >> 5) * 8 + i;
-                    w2f[(((size_t)b * KS + ks) * 64 + lane) * 8 + i] = bf16_half(em->w2[(size_t)k * Hd + n]);
-                }
-    for (int hbg = 0; hbg < Hd / 32; ++hbg)
-        for (int jj = 0; jj < 2; ++jj)
-            for (int lane = 0; lane < 64; ++lane)
-                for (int i = 0; i < 8; ++i) {
-                    const int g = lane >> 5, f = lane & 31;
-                    const int n = hbg * 32 + (jj * 2 + i / 4) * 8 + g * 4 + (i % 4);
-                    w3p[(((size_t)hbg * 2 + jj) * 64 + lane) * 8 + i] =
-                        f < 16 ? bf16_half(em->w3[(size_t)n * 16 + f]) : (uint16_t)0;
-                }
+    // The caller's weights ([in][out] bf16) are copied as they are and rearranged on the device
+    // into the network kernel's layouts (launch_pack_weights).
+    uint16_t *w1r, *w2r, *w3r;
     __bf16 *w1d, *w2d, *w3d, *wtd;
     double* tvd;
-    if ((rc = mem.alloc(&w1d, w1t.size(), "w1t"))) return rc;
-    if ((rc = mem.alloc(&w2d, w2f.size(), "w2f"))) return rc;
-    if ((rc = mem.alloc(&w3d, w3p.size(), "w3p"))) return rc;
+    if ((rc = mem.alloc(&w1r, (size_t)Hd * 16, "w1 (as given)"))) return rc;
+    if ((rc = mem.alloc(&w2r, (size_t)Hd * Hd, "w2 (as given)"))) return rc;
+    if ((rc = mem.alloc(&w3r, (size_t)Hd * 16, "w3 (as given)"))) return rc;
+    if ((rc = mem.alloc(&w1d, (size_t)Hd * 16, "w1t"))) return rc;
+    if ((rc = mem.alloc(&w2d, (size_t)Hd * Hd, "w2f"))) return rc;
+    if ((rc = mem.alloc(&w3d, (size_t)Hd * 32, "w3p"))) return rc;
     if ((rc = mem.alloc(&wtd, (size_t)em->temb_dim * Hd, "wt"))) return rc;
     if ((rc = mem.alloc(&tvd, (size_t)T, "t_values"))) return rc;
     if ((rc = mem.alloc(&d.temb, (size_t)T * Hd, "temb"))) return rc;
     d.nsplit = mlp_splits(Hd);
     if ((rc = mem.alloc(&d.Ep, (size_t)d.nsplit * ep_rows * Dz, "Ep"))) return rc;
-    PA_HIP(hipMemcpyAsync(w1d, w1t.data(), w1t.size() * 2, hipMemcpyHostToDevice, st));
-    PA_HIP(hipMemcpyAsync(w2d, w2f.data(), w2f.size() * 2, hipMemcpyHostToDevice, st));
-    PA_HIP(hipMemcpyAsync(w3d, w3p.data(), w3p.size() * 2, hipMemcpyHostToDevice, st));
+    PA_HIP(hipMemcpyAsync(w1r, em->w1, (size_t)Hd * 16 * 2, hipMemcpyHostToDevice, st));
+    PA_HIP(hipMemcpyAsync(w2r, em->w2, (size_t)Hd * Hd * 2, hipMemcpyHostToDevice, st));
+    PA_HIP(hipMemcpyAsync(w3r, em->w3, (size_t)Hd * 16 * 2, hipMemcpyHostToDevice, st));
     PA_HIP(hipMemcpyAsync(wtd, em->wt, (size_t)em->temb_dim * Hd * 2, hipMemcpyHostToDevice, st));
-    PA_HIP(hipMemcpyAsync(tvd, tv.data(), (size_t)T * sizeof(double), hipMemcpyHostToDevice, st));
+    PA_HIP(hipMemcpyAsync(tvd, tv, (size_t)T * sizeof(double), hipMemcpyHostToDevice, st));
+    PA_HIP(launch_pack_weights(w1r, w2r, w3r, Hd, w1d, w2d, w3d, st));
     d.w1t = w1d;
     d.w2f = w2d;
     d.w3p = w3d;
     PA_HIP(launch_temb_table(d, tvd, wtd, em->temb_dim, st));
-    PA_HIP(hipStreamSynchronize(st));   // host staging vectors die here
     return PA_OK;
 }
 

@@ -462,6 +462,67 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     }
 }
 
+namespace {
+
+// Half of a bf16 value on its bit pattern, rounded to nearest even. An exponent field of 2 or
+// more drops by one (exact). Below that (subnormals and the smallest binade) the magnitude
+// bits read as an integer are the value in units of 2^-133, which is halved with ties to even;
+// the result is again such a magnitude. NaN is returned quiet, infinity unchanged.
+__device__ __forceinline__ uint16_t bf16_half_bits(uint16_t b) {
+    const uint16_t sgn = b & 0x8000u, mag = b & 0x7fffu;
+    if (mag > 0x7f80u) return b | 0x0040u;
+    if (mag == 0x7f80u) return b;
+    if (mag >= 0x0100u) return sgn | (uint16_t)(mag - 0x0080u);
+    const uint16_t q = mag >> 1;
+    return sgn | (uint16_t)(q + ((mag & 1u) & (q & 1u)));
+}
+
+// Device layouts of the weights (grid-stride over the three outputs):
+//   w1t[n][f] = W1[f][n];
+//   w2f: W2^T as MFMA A fragments, fragment (b, ks) = lanes l = 0..63 x 8 values
+//        W2[16 ks + 8 (l/32) + i][32 b + l%32] / 2;
+//   w3p: fragment (hb, jj) = lanes l x 8 values W3[32 hb + (2 jj + i/4) 8 + 4 (l/32) + i%4][l%32] / 2
+//        for l%32 < 16, else 0 (the reduction index permuted to the GEMM2 accumulator layout).
+// W2 and W3 are stored halved because the kernel feeds them twice the GELU outputs.
+__global__ void k_pack_weights(const uint16_t* __restrict__ w1, const uint16_t* __restrict__ w2,
+                               const uint16_t* __restrict__ w3, int H, uint16_t* __restrict__ w1t,
+                               uint16_t* __restrict__ w2f, uint16_t* __restrict__ w3p) {
+    const size_t n1 = (size_t)H * 16, n2 = (size_t)H * H, n3 = (size_t)H * 32;
+    const int KS = H / 16;
+    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n1 + n2 + n3;
+         e += (size_t)gridDim.x * blockDim.x) {
+        if (e < n1) {
+            const int n = (int)(e / 16), f = (int)(e % 16);
+            w1t[e] = w1[(size_t)f * H + n];
+        } else if (e < n1 + n2) {
+            const size_t q = e - n1;
+            const int i = (int)(q & 7), lane = (int)((q >> 3) & 63);
+            const size_t frag = q >> 9;
+            const int ks = (int)(frag % KS), b = (int)(frag / KS);
+            const int n = b * 32 + (lane & 31), k = ks * 16 + (lane >> 5) * 8 + i;
+            w2f[q] = bf16_half_bits(w2[(size_t)k * H + n]);
+        } else {
+            const size_t q = e - n1 - n2;
+            const int i = (int)(q & 7), lane = (int)((q >> 3) & 63);
+            const size_t rest = q >> 9;
+            const int jj = (int)(rest & 1), hb = (int)(rest >> 1);
+            const int g = lane >> 5, f = lane & 31;
+            const int n = hb * 32 + (jj * 2 + i / 4) * 8 + g * 4 + (i % 4);
+            w3p[q] = f < 16 ? bf16_half_bits(w3[(size_t)n * 16 + f]) : (uint16_t)0;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_pack_weights(const uint16_t* w1, const uint16_t* w2, const uint16_t* w3, int H,
+                               __bf16* w1t, __bf16* w2f, __bf16* w3p, hipStream_t st) {
+    hipLaunchKernelGGL(k_pack_weights, dim3(1024), dim3(256), 0, st, w1, w2, w3, H,
+                       reinterpret_cast<uint16_t*>(w1t), reinterpret_cast<uint16_t*>(w2f),
+                       reinterpret_cast<uint16_t*>(w3p));
+    return hipGetLastError();
+}
+
 int mlp_supported(int hidden) { return hidden == 512 || hidden == 1024 || hidden == 2048; }
 
 int mlp_tokens_per_item() { return kTokMax; }

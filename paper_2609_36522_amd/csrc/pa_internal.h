@@ -89,6 +89,11 @@ constexpr size_t kFusedSlideMaxBytes = 256 * 1024;
 hipError_t launch_picard(const Dev& d, hipStream_t st, int linear, hipEvent_t start, hipEvent_t stop);
 // single: the launch evaluates at most one latent (64-token work items).
 hipError_t launch_eps_mlp(const Dev& d, hipStream_t st, hipEvent_t start, hipEvent_t stop, int single = 0);
+// Rearranges the patch-MLP weights ([in][out] bf16 bit patterns, device) into the network
+// kernel's layouts: w1t [H][16], w2f (W2^T fragments, halved), w3p (lane-permuted W3
+// fragments, halved).
+hipError_t launch_pack_weights(const uint16_t* w1, const uint16_t* w2, const uint16_t* w3, int H,
+                               __bf16* w1t, __bf16* w2f, __bf16* w3p, hipStream_t st);
 hipError_t launch_temb_table(const Dev& d, const double* t_values_dev, const __bf16* wt_dev,
                              int temb_dim, hipStream_t st);
 int picard_blocks(int D, int P);

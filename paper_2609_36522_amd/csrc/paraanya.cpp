@@ -3,8 +3,10 @@
 // the sweep enqueue loop. Every compute step of a sweep runs in the gfx950 kernels.
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <stddef.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -124,13 +126,20 @@ const char* paraanya_status_str(int s) {
     }
 }
 
-int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_t* schedule,
-                    int32_t window, double delta, double tol, const pa_eps_model_t* eps_model,
-                    void* stream, uint32_t flags, paraanya_t** out) {
-    pa::g_err.clear();
-    if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
-    *out = nullptr;
-    // ---- validation: no HIP call before this block completes
+}  // extern "C"
+
+namespace {
+
+// Validated arguments of a sampler request.
+struct Request {
+    int N, C, Hi, Wi, D, T, P;
+    double delta, tol, eta;
+    const pa_eps_model_t* em;
+};
+
+// Argument checks shared by paraanya_create and paraanya_sample_noalloc; no HIP call.
+int validate(const int32_t latent_shape[4], int32_t T, const pa_schedule_t* schedule, int32_t window,
+             double delta, double tol, const pa_eps_model_t* eps_model, Request* r) {
     if (!latent_shape || !schedule || !eps_model) return fail(PA_ERR_INVALID_ARG, "NULL argument");
     const int N = latent_shape[0], C = latent_shape[1], Hi = latent_shape[2], Wi = latent_shape[3];
     if (N < 1 || N > PA_MAX_BATCH) return fail(PA_ERR_INVALID_ARG, "batch N must be in [1, %d] (got %d)", PA_MAX_BATCH, N);
@@ -143,81 +152,99 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
         return fail(PA_ERR_INVALID_ARG, "window must be in [1, min(T, %d)]", PA_MAX_WINDOW);
     if (!(delta >= 0.0)) return fail(PA_ERR_INVALID_ARG, "delta must be >= 0 (got %g)", delta);
     if (!(tol >= 0.0)) return fail(PA_ERR_INVALID_ARG, "tol must be >= 0 (got %g)", tol);
+    int rc = pa::check_eps_model(eps_model, C, Hi, Wi, T);
+    if (rc) return rc;
+    *r = Request{N, C, Hi, Wi, (int)Dl, T, window, delta, tol, schedule->eta, eps_model};
+    return PA_OK;
+}
+
+// Geometry and device buffers of a handle (allocated, or carved from a workspace, by h->mem);
+// coef: the [T][3] step coefficients (host), tv: the T time values (host). The pinned host
+// mirror and progress words are the caller's business. Enqueues the uploads on h->stream.
+int setup_handle(paraanya* h, const Request& q, const double* coef, const double* tv) {
+    Dev& d = h->d;
+    d.N = q.N; d.T = q.T; d.P = q.P; d.D = q.D; d.C = q.C; d.Himg = q.Hi; d.Wimg = q.Wi;
+    d.delta = q.delta; d.tol = q.tol;
+    d.revisit_thr = 0.05;
+    d.picard_blocks = pa::picard_blocks(q.D, q.P);
+    h->model = q.em->kind;
+    int dev_id = 0;
+    PA_HIP(hipGetDevice(&dev_id));
+    int cus = 0;
+    PA_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev_id));
+    const size_t Dz = (size_t)q.D, Nz = (size_t)q.N, T = (size_t)q.T, P = (size_t)q.P;
+    int rc;
+    if ((rc = h->alloc(&d.X, Nz * (T + 1) * Dz, "X"))) return rc;
+    if ((rc = h->alloc(&d.Xh, Nz * T * Dz, "Xh"))) return rc;
+    if ((rc = h->alloc(&d.Eh, Nz * T * Dz, "Eh"))) return rc;
+    if ((rc = h->alloc(&d.valid, Nz * T, "valid"))) return rc;
+    if ((rc = h->alloc(&d.coef, 3 * T, "coef"))) return rc;
+    if ((rc = h->alloc(&d.part_res, Nz * P * d.picard_blocks, "part_res"))) return rc;
+    if ((rc = h->alloc(&d.part_dev, Nz * P * d.picard_blocks, "part_dev"))) return rc;
+    if ((rc = h->alloc(&d.ctrl, Nz, "ctrl"))) return rc;
+    // Fused sweep (network -> Picard, the slide computed by every block of the next network
+    // kernel): one sample, patch-MLP, and a partial-sum volume that a block reduces quickly.
+    d.fused_slide = (q.em->kind == PA_EPS_PATCH_MLP && q.N == 1 &&
+                     2 * P * d.picard_blocks * sizeof(double) <= pa::kFusedSlideMaxBytes) ? 1 : 0;
+    if ((rc = h->alloc(&d.pre, Nz, "pre"))) return rc;
+    if (h->flags & PA_FLAG_TRACE)
+        if ((rc = h->alloc(&d.trace, Nz * T, "trace"))) return rc;
+    if (q.eta > 0.0) {
+        if ((rc = h->alloc(&h->noise_buf, Nz * T * Dz, "noise"))) return rc;
+        d.noise = h->noise_buf;
+    }
+    // Whole network outputs written straight into the cache (unless split ones are forced).
+    if (q.em->kind == PA_EPS_PATCH_MLP && !(h->flags & PA_FLAG_SPLIT_OUTPUTS))
+        if ((rc = h->alloc(&d.eps_whole, 1, "eps_whole"))) return rc;
+    // setup_network takes all its buffers before it enqueues anything, so a request that does
+    // not fit fails before the first upload.
+    if ((rc = pa::setup_network(d, h->mem, q.em, tv, cus, Nz * P, h->stream))) return rc;
+    PA_HIP(hipMemcpyAsync(d.coef, coef, 3 * T * sizeof(double), hipMemcpyHostToDevice, h->stream));
+    return PA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_t* schedule,
+                    int32_t window, double delta, double tol, const pa_eps_model_t* eps_model,
+                    void* stream, uint32_t flags, paraanya_t** out) {
+    pa::g_err.clear();
+    if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    // ---- validation: no HIP call before this block completes
+    Request q;
+    int rc = validate(latent_shape, T, schedule, window, delta, tol, eps_model, &q);
+    if (rc) return rc;
     if (flags & ~(PA_FLAG_TRACE | PA_FLAG_PROFILE | PA_FLAG_PROFILE_SOLVER | PA_FLAG_SPLIT_OUTPUTS))
         return fail(PA_ERR_INVALID_ARG, "unknown flags");
-    const int D = (int)Dl;
-    const pa_eps_model_t* em = eps_model;
-    int rc = pa::check_eps_model(em, C, Hi, Wi, T);
-    if (rc) return rc;
     std::vector<double> ab, tv;
     if ((rc = pa::build_schedule(schedule, T, ab, tv))) return rc;
-    const double eta = schedule->eta;
-    std::vector<double> coef = pa::step_coefficients(ab, T, eta);
+    std::vector<double> coef = pa::step_coefficients(ab, T, q.eta);
 
     // ---- resources
     paraanya* h = new (std::nothrow) paraanya();
     if (!h) return fail(PA_ERR_OOM, "host allocation failed");
     h->stream = (hipStream_t)stream;
     h->flags = flags;
-    h->model = em->kind;
     h->coef_host = coef;
-    Dev& d = h->d;
-    d.N = N; d.T = T; d.P = window; d.D = D; d.C = C; d.Himg = Hi; d.Wimg = Wi;
-    d.delta = delta; d.tol = tol;
-    d.revisit_thr = 0.05;
-    d.picard_blocks = pa::picard_blocks(D, window);
     auto bail = [&](int code) { delete h; return code; };
-
-    int dev_id = 0;
-    hipError_t he = hipGetDevice(&dev_id);
-    if (he != hipSuccess) return bail(hip_fail(he, "hipGetDevice"));
-    int cus = 0;
-    he = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev_id);
-    if (he != hipSuccess) return bail(hip_fail(he, "hipDeviceGetAttribute"));
-
-    const size_t Dz = (size_t)D;
-    const size_t Nz = (size_t)N;
-    if ((rc = h->alloc(&d.X, Nz * (T + 1) * Dz, "X"))) return bail(rc);
-    if ((rc = h->alloc(&d.Xh, Nz * T * Dz, "Xh"))) return bail(rc);
-    if ((rc = h->alloc(&d.Eh, Nz * T * Dz, "Eh"))) return bail(rc);
-    if ((rc = h->alloc(&d.valid, Nz * T, "valid"))) return bail(rc);
-    if ((rc = h->alloc(&d.coef, 3 * (size_t)T, "coef"))) return bail(rc);
-    if ((rc = h->alloc(&d.part_res, Nz * window * d.picard_blocks, "part_res"))) return bail(rc);
-    if ((rc = h->alloc(&d.part_dev, Nz * window * d.picard_blocks, "part_dev"))) return bail(rc);
-    if ((rc = h->alloc(&d.ctrl, Nz, "ctrl"))) return bail(rc);
-    // Fused sweep (network -> Picard, the slide computed by every block of the next network
-    // kernel): one sample, patch-MLP, and a partial-sum volume that a block reduces quickly.
-    d.fused_slide = (em->kind == PA_EPS_PATCH_MLP && N == 1 &&
-                     2 * (size_t)window * d.picard_blocks * sizeof(double) <= pa::kFusedSlideMaxBytes) ? 1 : 0;
-    if ((rc = h->alloc(&d.pre, Nz, "pre"))) return bail(rc);
-    if (flags & PA_FLAG_TRACE)
-        if ((rc = h->alloc(&d.trace, Nz * T, "trace"))) return bail(rc);
-    if (eta > 0.0) {
-        if ((rc = h->alloc(&h->noise_buf, Nz * T * Dz, "noise"))) return bail(rc);
-        d.noise = h->noise_buf;
-    }
-    he = hipHostMalloc((void**)&h->ctrl_host, Nz * sizeof(Ctrl), hipHostMallocDefault);
+    if ((rc = setup_handle(h, q, coef.data(), tv.data()))) return bail(rc);
+    Dev& d = h->d;
+    const size_t Nz = (size_t)q.N;
+    hipError_t he = hipHostMalloc((void**)&h->ctrl_host, Nz * sizeof(Ctrl), hipHostMallocDefault);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostMalloc"));
     memset(h->ctrl_host, 0, Nz * sizeof(Ctrl));
     he = hipHostMalloc((void**)&h->progress_host, Nz * sizeof(uint64_t) < 256 ? 256 : Nz * sizeof(uint64_t),
                        hipHostMallocMapped | hipHostMallocCoherent);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostMalloc(progress)"));
-    for (int n = 0; n < N; ++n) h->progress_host[n] = 0;
+    for (size_t n = 0; n < Nz; ++n) h->progress_host[n] = 0;
     he = hipHostGetDevicePointer((void**)&d.progress, h->progress_host, 0);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostGetDevicePointer"));
-
-#define PA_HIP_BAIL(call)                                        \
-    do {                                                         \
-        hipError_t e_ = (call);                                  \
-        if (e_ != hipSuccess) return bail(hip_fail(e_, #call));  \
-    } while (0)
-
-    PA_HIP_BAIL(hipMemcpyAsync(d.coef, coef.data(), coef.size() * sizeof(double), hipMemcpyHostToDevice, h->stream));
-    if ((rc = pa::setup_network(d, h->mem, em, tv, cus, Nz * window, h->stream))) return bail(rc);
-    // Whole network outputs written straight into the cache (unless split ones are forced).
-    if (em->kind == PA_EPS_PATCH_MLP && !(flags & PA_FLAG_SPLIT_OUTPUTS))
-        if ((rc = h->alloc(&d.eps_whole, 1, "eps_whole"))) return bail(rc);
-#undef PA_HIP_BAIL
+    // The host vectors above die at return: wait for the uploads that read them.
+    he = hipStreamSynchronize(h->stream);
+    if (he != hipSuccess) return bail(hip_fail(he, "hipStreamSynchronize"));
     *out = h;
     return PA_OK;
 }
@@ -482,5 +509,137 @@ int paraanya_kernel_times(paraanya_t* h, pa_ktimes_t* out) {
 }
 
 void paraanya_destroy(paraanya_t* h) { delete h; }
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------- no allocation
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+// Workspace of paraanya_sample_noalloc. Every device the library runs on holds its own copy
+// until the process ends. In host code the name stands for a host-side shadow, not a device
+// address: host code uses only the device address hipGetSymbolAddress returns for the
+// current device (g_scratch_addr), for the kernels' arguments and every copy.
+static __device__ __align__(256) unsigned char scratch[PA_NOALLOC_WORKSPACE_BYTES];
+
+std::mutex g_scratch_lock[kMaxDevices];   // one call at a time per device shares the workspace
+void* g_scratch_addr[kMaxDevices];        // device address of scratch, per device (under the lock)
+
+// Leading fields of a control block (the counters and the window), read back at the end.
+constexpr size_t kCtrlHead = offsetof(Ctrl, miss_idx);
+
+}  // namespace
+
+extern "C" {
+
+int paraanya_sample_noalloc(const int32_t latent_shape[4], int32_t T, const pa_schedule_t* schedule,
+                            int32_t window, double delta, double tol, const pa_eps_model_t* eps_model,
+                            void* stream, const float* x_init, float* x_out, pa_stats_t* stats) {
+    pa::g_err.clear();
+    if (!x_init || !x_out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
+    Request q;
+    int rc = validate(latent_shape, T, schedule, window, delta, tol, eps_model, &q);
+    if (rc) return rc;
+    if (T > PA_NOALLOC_MAX_STEPS)
+        return fail(PA_ERR_INVALID_ARG, "allocation-free sampling: T must be at most %d (got %d)", PA_NOALLOC_MAX_STEPS, T);
+    if (schedule->eta != 0.0)
+        return fail(PA_ERR_UNSUPPORTED, "allocation-free sampling: only the deterministic step (eta = 0) is built");
+    // Schedule tables on the stack (no host allocation either).
+    double ab[PA_NOALLOC_MAX_STEPS + 1], tv[PA_NOALLOC_MAX_STEPS], coef[3 * PA_NOALLOC_MAX_STEPS];
+    if ((rc = pa::build_schedule(schedule, T, ab, tv))) return rc;
+    pa::step_coefficients(ab, T, 0.0, coef);
+
+    int dev = 0;
+    PA_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(PA_ERR_UNSUPPORTED, "allocation-free sampling: device %d beyond the first %d", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_lock[dev]);
+    if (!g_scratch_addr[dev]) {
+        void* p = nullptr;
+        PA_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));   // this device's copy
+        if (!p) return fail(PA_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+        g_scratch_addr[dev] = p;
+    }
+
+    // A handle on the stack: its containers stay empty; every buffer is carved from the
+    // workspace in order (the carve fails before anything is enqueued if it does not fit).
+    paraanya h;
+    h.stream = (hipStream_t)stream;
+    h.flags = 0;
+    h.mem.workspace(g_scratch_addr[dev], PA_NOALLOC_WORKSPACE_BYTES);
+    Dev& d = h.d;
+    const size_t Nz = (size_t)q.N;
+    if ((rc = h.alloc(&d.progress, Nz, "progress"))) return rc;
+    if ((rc = setup_handle(&h, q, coef, tv))) return rc;
+
+    // Reset. The workspace keeps the previous call's contents: the progress words are
+    // cleared here; the reset kernel clears the cache flags and the control blocks.
+    const size_t row = (size_t)q.D * sizeof(float);
+    PA_HIP(hipMemsetAsync(d.progress, 0, Nz * sizeof(uint64_t), h.stream));
+    PA_HIP(hipMemcpy2DAsync(d.X, (size_t)(T + 1) * row, x_init, row, row, Nz, hipMemcpyDeviceToDevice, h.stream));
+    PA_HIP(pa::launch_reset(d, h.stream));
+    h.have_reset = true;
+
+    // Sweeps in batches: the progress words are device memory here, so the host reads them
+    // back after each batch and enqueues the ceil((T - s)/P) sweeps that the slowest sample
+    // certainly still needs (at least one). A fused sweep publishes its slide from the next
+    // network kernel, so one sweep beyond T may be needed; later sweeps exit at once.
+    const int cap = T + (d.fused_slide ? 1 : 0);
+    int enqueued = 0, need = (T + q.P - 1) / q.P;
+    uint64_t words[PA_MAX_BATCH];
+    for (;;) {
+        const int k = need < cap - enqueued ? need : cap - enqueued;
+        if (k <= 0) return fail(PA_ERR_HIP, "sampler did not finish within T sweeps");
+        for (int i = 0; i < k; ++i)
+            if ((rc = h.enqueue_sweep())) return rc;
+        enqueued += k;
+        PA_HIP(hipMemcpyAsync(words, d.progress, Nz * sizeof(uint64_t), hipMemcpyDeviceToHost, h.stream));
+        PA_HIP(hipStreamSynchronize(h.stream));
+        bool all = true;
+        need = 1;
+        for (size_t n = 0; n < Nz; ++n) {
+            if ((words[n] >> 31) & 1u) continue;
+            all = false;
+            const int s_now = (int)(words[n] & 0x7fffffffu);
+            const int qn = (T - s_now + q.P - 1) / q.P;
+            if (qn > need) need = qn;
+        }
+        if (all) break;
+    }
+    // Every sample is done; the slide that published that also wrote its control block.
+    h.slide_pending = false;
+    PA_HIP(hipMemcpy2DAsync(x_out, row, d.X + (size_t)T * q.D, (size_t)(T + 1) * row, row, Nz,
+                            hipMemcpyDeviceToDevice, h.stream));
+    unsigned char heads[PA_MAX_BATCH][kCtrlHead];
+    PA_HIP(hipMemcpy2DAsync(heads, kCtrlHead, d.ctrl, sizeof(Ctrl), kCtrlHead, Nz, hipMemcpyDeviceToHost, h.stream));
+    PA_HIP(hipStreamSynchronize(h.stream));
+    bool nonfinite = false;
+    pa_stats_t agg{};
+    for (size_t n = 0; n < Nz; ++n) {
+        Ctrl c;
+        memcpy(&c, heads[n], kCtrlHead);
+        pa_stats_t o;
+        fill_stats(c, &o);
+        nonfinite = nonfinite || o.nonfinite;
+        if (n == 0) {
+            agg = o;
+            continue;
+        }
+        agg.nfe += o.nfe;
+        agg.hits += o.hits;
+        agg.misses += o.misses;
+        agg.revisits += o.revisits;
+        agg.revisits_below += o.revisits_below;
+        if (o.sweeps > agg.sweeps) agg.sweeps = o.sweeps;
+        if (o.window_start < agg.window_start) agg.window_start = o.window_start;
+        if (o.window_end < agg.window_end) agg.window_end = o.window_end;
+        agg.done = agg.done && o.done;
+        agg.nonfinite = agg.nonfinite || o.nonfinite;
+    }
+    if (stats) *stats = agg;
+    if (nonfinite) return fail(PA_ERR_NONFINITE, "non-finite residual during sampling");
+    return PA_OK;
+}
 
 }  // extern "C"

@@ -179,8 +179,10 @@ int paraanya_parareal_create(const int32_t latent_shape[4], int32_t T, const pa_
     if (he != hipSuccess) return bail(hip_fail(he, "hipMemcpyAsync(pr_coef)"));
     he = hipMemsetAsync(d.ctrl, 0, Bz * sizeof(Ctrl), h->stream);
     if (he != hipSuccess) return bail(hip_fail(he, "hipMemsetAsync(ctrl)"));
-    // setup_network synchronizes the stream, so the host vectors above may die after it.
-    if ((rc = pa::setup_network(d, m, eps_model, tv, cus, Bz, h->stream))) return bail(rc);
+    if ((rc = pa::setup_network(d, m, eps_model, tv.data(), cus, Bz, h->stream))) return bail(rc);
+    // The host vectors above die at return: wait for the copies that read them.
+    he = hipStreamSynchronize(h->stream);
+    if (he != hipSuccess) return bail(hip_fail(he, "hipStreamSynchronize"));
     *out = h;
     return PA_OK;
 }

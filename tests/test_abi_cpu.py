@@ -22,7 +22,7 @@ def _declared():
 def test_library_exports_every_declared_symbol():
     lib = B.load_library()
     names = _declared()
-    assert len(names) == 25
+    assert len(names) == 26
     assert sorted(B.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -197,3 +197,26 @@ def test_parareal_null_handle_calls_fail_cleanly():
     assert lib.paraanya_parareal_residuals(None, 0, None) == B.PA_ERR_INVALID_ARG
     assert lib.paraanya_parareal_read_boundaries(None, None) == B.PA_ERR_INVALID_ARG
     lib.paraanya_parareal_destroy(None)
+
+
+@pytest.mark.parametrize("kw,code,frag", [
+    (dict(T=1025), B.PA_ERR_INVALID_ARG, "at most 1024"),
+    (dict(eta=0.5), B.PA_ERR_UNSUPPORTED, "eta"),
+    (dict(window=0), B.PA_ERR_INVALID_ARG, "window"),
+    (dict(null_x=True), B.PA_ERR_INVALID_ARG, "NULL"),
+])
+def test_noalloc_rejects_before_any_hip_call(kw, code, frag):
+    """The allocation-free entry point checks its arguments and limits before any HIP call."""
+    lib = B.load_library()
+    T = kw.get("T", 10)
+    sh = (C.c_int32 * 4)(1, 4, 8, 8)
+    sc = B.Schedule(B.PA_SCHED_SCALED_LINEAR, 0.00085, 0.012, 1000 if T <= 1000 else 2000, 0, 1, None, None,
+                    kw.get("eta", 0.0))
+    c = np.ones(T, np.float32)
+    em = B.EpsModel(B.PA_EPS_LINEAR, c.ctypes.data_as(C.POINTER(C.c_float)), 0, 0, 0, None, None, None, None)
+    x = None if kw.get("null_x") else C.c_void_p(16)
+    st = B.Stats()
+    rc = lib.paraanya_sample_noalloc(sh, T, C.byref(sc), kw.get("window", 4), 0.05, 1e-3, C.byref(em), None,
+                                     x, C.c_void_p(16), C.byref(st))
+    assert rc == code, (rc, lib.paraanya_last_error())
+    assert frag in lib.paraanya_last_error().decode()
