@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <chrono>
+
 #include <hip/hip_ext.h>
 
 namespace pa {
@@ -112,6 +114,15 @@ int check_eps_model(const pa_eps_model_t* em, int C, int Hi, int Wi, int T) {
         return fail(PA_ERR_INVALID_ARG, "unknown eps model kind %d", em->kind);
     }
     return PA_OK;
+}
+
+bool QueryPacer::due() {
+    const int64_t now = std::chrono::duration_cast<std::chrono::nanoseconds>(
+                            std::chrono::steady_clock::now().time_since_epoch()).count();
+    if (next_ns == 0) next_ns = now + kIntervalNs;   // the first query one interval from now
+    if (now < next_ns) return false;
+    next_ns = now + kIntervalNs;
+    return true;
 }
 
 int KernelTimer::pair(int k, hipEvent_t* e0, hipEvent_t* e1) {

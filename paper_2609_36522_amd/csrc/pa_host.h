@@ -80,6 +80,16 @@ struct DevMem {
     }
 };
 
+// Rate limit for polling a stream while the host spins on a progress word: hipStreamQuery on a
+// stream with queued kernels delays the next dispatch on it (measured: ~5.5 us gaps between
+// kernels that otherwise run back to back), so a waiting loop asks at most once per interval
+// (and only to notice a failed or idle stream; progress itself comes from the word).
+struct QueryPacer {
+    static constexpr int64_t kIntervalNs = 1000000;   // 1 ms
+    int64_t next_ns = 0;
+    bool due();                        // true at most once per interval
+};
+
 // Start/stop event pairs attached to kernel dispatches (hipExtLaunchKernelGGL), summed per
 // kernel kind when drained. A pair's interval can include idle time between the kernel and
 // the work before it on the stream.

@@ -313,8 +313,8 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
     // certainly still needs (s advances by at most P per sweep) -- and stops enqueuing once
     // every sample is done. Sweeps enqueued after that exit at their first instruction. Every
     // sweep advances each unfinished sample's s by at least 1, so at most T sweeps are ever
-    // enqueued (T + 1 for a fused sweep, see below). The stream is polled while waiting, so a
-    // failed or idle stream ends the loop.
+    // enqueued (T + 1 for a fused sweep, see below). The stream is polled (at most once per
+    // millisecond, see QueryPacer) while waiting, so a failed or idle stream ends the loop.
     constexpr int kLookahead = 2;
     volatile uint64_t* prog = h->progress_host;
     auto scan = [&](int* completed, int* need) {      // returns true once all are done
@@ -336,6 +336,7 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
     // the sample is followed by one more (its network kernel only computes that slide).
     const int cap = T + (h->d.fused_slide ? 1 : 0);
     int enqueued = 0;
+    pa::QueryPacer pacer;
     for (unsigned spin = 0;; ++spin) {
         int completed, need;
         if (scan(&completed, &need)) break;
@@ -347,7 +348,7 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
             enqueued += k;
             continue;
         }
-        if (spin % 256 != 255) continue;        // poll the stream now and then, not per spin
+        if (spin % 64 != 63 || !pacer.due()) continue;   // poll the stream rarely, not per spin
         const hipError_t q = hipStreamQuery(h->stream);
         if (q == hipSuccess) {
             // Stream idle: the words are final for the enqueued work.

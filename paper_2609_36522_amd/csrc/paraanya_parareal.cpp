@@ -75,10 +75,11 @@ struct paraanya_parareal {
     // Waits for the convergence word of iteration k; returns 1 if done, 0 if not, < 0 on error.
     int wait_iteration(int k) {
         volatile uint64_t* w = progress_host;
+        pa::QueryPacer pacer;
         for (unsigned spin = 0;; ++spin) {
             const uint64_t v = *w;
             if ((int)(v >> 32) >= k + 1) return (v >> 31) & 1u ? 1 : 0;
-            if (spin % 256 != 255) continue;
+            if (spin % 64 != 63 || !pacer.due()) continue;
             const hipError_t q = hipStreamQuery(stream);
             if (q == hipSuccess) {
                 const uint64_t v2 = *w;

@@ -34,7 +34,16 @@ STATE_ULPS = 1              # per-sweep updated states, in fp32 ulps of the orac
 STATE_FRAC = 1e-4           # at most this fraction of state elements may differ at all
 FINAL_RTOL = 1e-4           # final latent, max-abs x RMS
 SUM_RTOL = 1e-11            # deviations/residuals: fp64 sums in different orders
-EPS_RTOL = 1e-2             # fresh network outputs, max-abs x RMS (bf16 rounding flips)
+# Fresh network outputs: max-abs error <= EPS_RTOL x the larger of the output's RMS over the
+# latent and the largest magnitude among the 16 outputs of the same token (eps_error). Both
+# sides round every activation to bf16; the device accumulates in fp32, the oracle in fp64, so
+# an activation near a bf16 rounding boundary can round differently, and its step (half a bf16
+# ulp, proportional to the activation) moves that token's outputs by an amount proportional to
+# the token's own scale. Seen on the device: one token of a late state (latent RMS 12) with
+# activations up to 79 (bf16 step 0.5) deviated by 1.01e-2 x the latent RMS, 2.3e-3 x its own
+# output scale; a CPU evaluation of the same latent with fp32 accumulation and the exact erf
+# GELU deviates from the oracle by the same 1.01e-2 there, so the deviation is the arithmetic's.
+EPS_RTOL = 1e-2
 REVISIT_THR = 0.05          # default threshold of the device's revisit counters
 # An oracle trajectory of its own (follow) stores its own fp32 states, which may differ from
 # the device's by one rounding in a few elements (the step-locked check allows that); an
@@ -58,6 +67,15 @@ def oracle_network(wl, t_values):
 def rms(a) -> float:
     a = np.asarray(a, dtype=np.float64)
     return float(np.sqrt(np.mean(a * a))) if a.size else 0.0
+
+
+def eps_error(got, ref, shape) -> float:
+    """Largest |got - ref| of a network output (flat [D]) relative to max(RMS of ref, the
+    largest |ref| among the outputs of the same token): the quantity EPS_RTOL bounds."""
+    ref = np.asarray(ref, np.float64).reshape(shape)
+    d = np.abs(np.asarray(got, np.float64).reshape(shape) - ref)
+    scale = np.maximum(np.abs(em.patchify(ref, 2)).max(axis=1), max(rms(ref), 1e-30))
+    return float((em.patchify(d, 2).max(axis=1) / scale).max())
 
 
 class Log:
@@ -241,10 +259,9 @@ class Run:
                 if not pick:
                     continue
                 ref = self.net.eval_one(X_before[t - sw], t)
-                sc = max(rms(ref), 1e-30)
-                e_rel = float(np.max(np.abs(gpu_eps[t].astype(np.float64) - ref)) / sc)
+                e_rel = eps_error(gpu_eps[t], ref, self.wl.latent)
                 self.eps_err.append(e_rel)
-                assert e_rel <= EPS_RTOL, f"sample {n} sweep {k}: network output of {t} off by {e_rel:.3g} x RMS"
+                assert e_rel <= EPS_RTOL, f"sample {n} sweep {k}: network output of {t} off by {e_rel:.3g} x its scale"
         self.records[n].append(g)
         if self.keep_eps and self.wl.model != "linear":
             self.eps_rows[n].append(gpu_eps)
@@ -296,7 +313,7 @@ class Run:
         return err
 
     def eps_summary(self) -> str:
-        """Count, maximum and 99th percentile of the checked network-output errors."""
+        """Count, maximum and 99th percentile of the checked network-output errors (eps_error)."""
         if not self.eps_err:
             return "eps_checked=0"
         e = np.asarray(self.eps_err)

@@ -5,7 +5,8 @@ device's own pre-sweep state (step-locked) and then follows its own trajectory f
 same initial latent. Decisions must agree except inside the 1e-6 relative band around
 delta/tau; final latents agree within 1e-4 x RMS. Fresh patch-MLP outputs are compared one
 by one with the oracle network (every output of a run, or every output of its first sweep
-and a fixed stride after that for the largest runs), within 1e-2 x RMS.
+and a fixed stride after that for the largest runs), within 1e-2 x the larger of the
+output's RMS and the token's own output scale (parity_harness.eps_error).
 """
 import math
 import sys

@@ -208,3 +208,23 @@ def test_patch_mlp_matches_explicit_loops():
         # can flip a rare bf16 rounding: allow a few bf16 steps of one activation.
         assert np.max(np.abs(got - ref)) <= 2e-3 * scale
         assert np.mean(got == ref) > 0.9
+
+
+def test_eps_error_scale_is_rms_or_the_tokens_own():
+    """The network-output parity measure: max |got - ref| over max(RMS, the token's largest
+    |ref|); a token whose outputs exceed the RMS is measured against its own scale."""
+    import parity_harness as H
+    shape = (4, 4, 4)
+    ref = np.ones(shape, np.float64)
+    got = ref.copy()
+    got[0, 0, 0] += 0.01                       # token 0, RMS 1 -> 0.01
+    assert H.eps_error(got, ref, shape) == pytest.approx(0.01)
+    ref2 = ref.copy()
+    ref2[:, 0:2, 0:2] = 10.0                   # token 0's outputs are 10: its scale is 10
+    got2 = ref2.copy()
+    got2[0, 0, 0] += 0.1
+    rms2 = np.sqrt(np.mean(ref2 ** 2))
+    assert H.eps_error(got2, ref2, shape) == pytest.approx(0.01)
+    got3 = ref2.copy()
+    got3[0, 2, 2] += 0.1                       # another token, scale max(1, RMS) = RMS
+    assert H.eps_error(got3, ref2, shape) == pytest.approx(0.1 / rms2)
