@@ -1,9 +1,10 @@
 """Build libparaanya.so (gfx950) in-tree with hipcc.
 
-    python -m paper_2609_36522_amd.build
+    python -m paper_2609_36522_amd.build [--sanitized]
 
 Compiles the HIP kernels and the host library into one shared object next to this
-file. Packed-fp32 VALU instructions are disabled for every device compilation.
+file. Packed-fp32 VALU instructions are disabled for every device compilation. With
+--sanitized it also builds the host-sanitized copy and the ABI driver the tests run.
 """
 from __future__ import annotations
 
@@ -37,22 +38,63 @@ def command(out: str = LIB) -> list:
             "-I", INCLUDE, "-I", CSRC, *srcs, "-o", out]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and atomically replace the library. Returns its path."""
-    tmp = LIB + ".tmp"
-    cmd = command(tmp)
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    msgs = "\n".join(line for line in (r.stdout + r.stderr).splitlines()
+# Host-sanitized copy of the library (AddressSanitizer + UndefinedBehaviorSanitizer on the host
+# code only; every sanitizer flag is scoped to the host compilation, the device code is built as
+# for the library) and the C driver that exercises its ABI (tests/sanitize/abi_driver.cpp).
+SAN_DIR = os.path.join(ROOT, "tests", "sanitize", "_build")
+SAN_LIB = os.path.join(SAN_DIR, "libparaanya_san.so")
+SAN_DRIVER = os.path.join(SAN_DIR, "abi_driver")
+SAN_DRIVER_SRC = os.path.join(ROOT, "tests", "sanitize", "abi_driver.cpp")
+_HOST_SAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def sanitized_commands() -> tuple:
+    """(library command, driver command) of the host-sanitized build."""
+    lib = command(SAN_LIB + ".tmp")
+    lib = lib[:-2] + ["-g", *_HOST_SAN] + lib[-2:]
+    drv = [hipcc(), "-O1", "-g", "-std=c++17", *_HOST_SAN, "-I", INCLUDE, SAN_DRIVER_SRC,
+           "-L", SAN_DIR, "-lparaanya_san", f"-Wl,-rpath,{SAN_DIR}", "-o", SAN_DRIVER + ".tmp"]
+    return lib, drv
+
+
+def _finish(r, what: str, verbose: bool) -> None:
+    out, err = r.communicate() if hasattr(r, "communicate") else (r.stdout, r.stderr)
+    msgs = "\n".join(line for line in ((out or "") + (err or "")).splitlines()
                      if "packed-fp32-ops" not in line)
     if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{msgs}")
+        raise RuntimeError(f"{what}: hipcc failed ({r.returncode}):\n{msgs}")
     if verbose and msgs.strip():
         print(msgs, flush=True)
+
+
+def build(verbose: bool = False, sanitized: bool = False) -> str:
+    """Compile every source and atomically replace the library. Returns its path.
+
+    sanitized: also build the host-sanitized library and its ABI driver (the two library
+    builds run side by side)."""
+    tmp = LIB + ".tmp"
+    cmd = command(tmp)
+    procs = [(subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True), "library", cmd)]
+    if sanitized:
+        os.makedirs(SAN_DIR, exist_ok=True)
+        lib_cmd, _ = sanitized_commands()
+        procs.append((subprocess.Popen(lib_cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True),
+                      "sanitized library", lib_cmd))
+    for p, what, c in procs:
+        if verbose:
+            print(" ".join(c), flush=True)
+        _finish(p, what, verbose)
     os.replace(tmp, LIB)
+    if sanitized:
+        os.replace(SAN_LIB + ".tmp", SAN_LIB)
+        _, drv_cmd = sanitized_commands()
+        if verbose:
+            print(" ".join(drv_cmd), flush=True)
+        _finish(subprocess.run(drv_cmd, capture_output=True, text=True), "sanitizer driver", verbose)
+        os.replace(SAN_DRIVER + ".tmp", SAN_DRIVER)
     return LIB
 
 
 if __name__ == "__main__":
-    print(build(verbose="-q" not in sys.argv))
+    print(build(verbose="-q" not in sys.argv, sanitized="--sanitized" in sys.argv))
