@@ -341,3 +341,47 @@ def test_create_out_of_memory_fails_cleanly(gpu_lib):
     with B.from_workload(wl) as s:
         out = s.sample(_x(wl)).cpu().numpy()
         assert s.stats()["done"] and np.isfinite(out).all()
+
+
+def test_largest_handle_offsets(gpu_lib):
+    """Maximum sizes: 64 samples (PA_MAX_BATCH), window 256 (PA_MAX_WINDOW), T = 1000 and 4x96x96
+    latents, so the trajectory alone holds 64 x 1001 x 36864 = 2.36e9 floats (beyond 2^31): a
+    32-bit element offset anywhere in a kernel or a host copy would read or write another
+    sample's rows. tau = inf makes every window converge in one sweep (slides of 256), delta =
+    0.05. Linear network: the last and the first sample end on the oracle's final latent (same
+    NFE and hits). Patch-MLP (H = 1024): the last sample's cached outputs at the last timesteps
+    equal the oracle network's outputs for the device's cached inputs, and its final latent
+    differs from the first sample's."""
+    from oracle import sampler as sp
+    import parity_harness as H
+    N, T, P = B.PA_MAX_BATCH, 1000, B.PA_MAX_WINDOW
+    shape = (4, 96, 96)
+    D = int(np.prod(shape))
+    assert N * (T + 1) * D > 2 ** 31
+    ab, tv = sch.sampler_alpha_bar(T)
+    alpha, b = sch.ddim_coefficients(ab)
+    xs = inputs.x_init_batch(shape, N).reshape(N, -1)
+    x = torch.from_numpy(xs.reshape(-1)).cuda()
+    lin = W.Workload("lin_64x4x96x96_T1000_P256", shape, T, P, 0.05, math.inf, "linear")
+    print(f"[max-size] linear N={N} T={T} P={P} latent={shape}", flush=True)
+    with B.from_workload(lin, batch=N) as s:
+        out = s.sample(x).cpu().numpy().reshape(N, -1)
+        st = [s.stats(n) for n in (0, N - 1)]
+    c = inputs.linear_coefficients(T)
+    for k, n in enumerate((0, N - 1)):
+        xo, _, ost = sp.sample(xs[n], T, P, 0.05, math.inf, alpha, b, em.linear_eps(c))
+        assert (st[k]["nfe"], st[k]["hits"]) == (ost.nfe, ost.hits), (n, st[k], ost)
+        rms = float(np.sqrt(np.mean(xo.astype(np.float64) ** 2)))
+        assert np.max(np.abs(out[n].astype(np.float64) - xo)) <= 1e-4 * rms, n
+    del out
+    mlp = W.Workload("mlp_64x4x96x96_T1000_P256_H1024", shape, T, P, 0.05, math.inf, "patch_mlp", hidden=1024)
+    print(f"[max-size] patch-MLP H=1024 N={N} T={T} P={P} latent={shape}", flush=True)
+    net = em.PatchMLP(inputs.mlp_weights(1024), tv, shape)
+    with B.from_workload(mlp, batch=N) as s:
+        out = s.sample(x).cpu().numpy().reshape(N, -1)
+        _, Xh, Eh, valid = s.read_state(T - 2, T, N - 1)
+    assert valid.all()
+    for i, t in enumerate((T - 2, T - 1)):
+        ref = net.eval_one(Xh[i], t)
+        assert H.eps_error(Eh[i], ref, shape) <= H.EPS_RTOL, t
+    assert np.isfinite(out).all() and not np.array_equal(out[0], out[N - 1])
