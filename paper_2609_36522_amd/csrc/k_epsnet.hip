@@ -149,6 +149,9 @@ __global__ __launch_bounds__(kWaves * 64) void k_eps_mlp(Dev d) {
     __shared__ int fmiss[PA_MAX_WINDOW];
     __shared__ int fnewest;
     if (d.fused_slide) {
+        // A launch queued after the one that finished the sample (that launch computed the last
+        // slide and published done) has nothing to do: every block leaves at once.
+        if (d.ctrl->done) return;
         static_assert(sizeof(SlideScratch) + 16 + kSlideSubDoubles * sizeof(double) <= sizeof(h1s),
                       "slide scratch must fit");
         SlideScratch& sc = *reinterpret_cast<SlideScratch*>(&h1s[0][0]);
