@@ -127,9 +127,9 @@ def timed_samples(sampler, x, steps, warmup, torch, profiled):
     t0 = time.perf_counter()
     for _ in range(steps):
         ts = time.perf_counter()
-        sampler.sample(x, out)                      # returns after the stream is synchronized
+        sampler.sample(x, out)                      # returns once every sample is done
         per_sample.append(time.perf_counter() - ts)
-        st = sampler.stats()                        # host mirror of the last synchronization
+        st = sampler.stats()                        # final counters, taken from the done words
         sweeps += st["sweeps"]
         nfe += st["nfe"]
         hits += st["hits"]

@@ -218,13 +218,20 @@ PA_API int paraanya_set_revisit_threshold(paraanya_t* h, double threshold);
 PA_API int paraanya_sweep(paraanya_t* h, int32_t* done);
 
 /* reset, sweeps until every sample is done, then x_out (device, N x D fp32) <- state T of
- * each sample. Returns after x_out
- * is written (the stream is synchronized). x_init and x_out may alias. The host does not
- * synchronize per sweep: it follows a progress word that each sweep writes to pinned host
- * memory and keeps a few sweeps queued ahead; sweeps queued past the end exit at once. */
+ * each sample. x_init and x_out may alias. The host does not synchronize per sweep: it
+ * follows a progress word that each sweep writes to pinned host memory and keeps a few sweeps
+ * queued ahead; sweeps queued past the end exit at once. The call returns once every sample
+ * is done, without draining the stream: the copy into x_out (and the tail of the last
+ * kernels) is queued on the stream, so work the caller enqueues on that stream afterwards
+ * sees x_out; synchronize the stream before reading x_out any other way. The final counters
+ * come with the done words, so paraanya_stats / paraanya_stats_sample right after return
+ * them without synchronizing; every other query synchronizes first. With PA_FLAG_PROFILE
+ * (or if the counter words are not yet visible) the call synchronizes before returning.
+ * NONFINITE as paraanya_sweep. */
 PA_API int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out);
 
-/* Counters and window position; synchronizes the stream. STATE before the first reset.
+/* Counters and window position; synchronizes the stream (not right after paraanya_sample,
+ * whose counters are already final). STATE before the first reset.
  * paraanya_stats aggregates over the samples (see pa_stats_t); paraanya_stats_sample
  * reports sample n alone (INVALID_ARG for n outside [0, N)). */
 PA_API int paraanya_stats(paraanya_t* h, pa_stats_t* out);

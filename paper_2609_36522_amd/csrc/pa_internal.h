@@ -57,7 +57,9 @@ struct Dev {
     Ctrl* ctrl;                // [N]
     SlidePre* pre;             // [N] pre-slide snapshots (fused sweep), or null
     int32_t fused_slide;       // 1: the network kernel computes the slide (N = 1), no k_slide
-    uint64_t* progress;        // [N] host-mapped words: sweeps << 32 | done << 31 | s
+    uint64_t* progress;        // [N] host-mapped words: sweeps << 32 | done << 31 | nonfinite << 30 | s
+    uint64_t* counters;        // [N][4] host-mapped final counters (epoch << 40 | value) or null
+    uint32_t epoch;            // sample epoch of the counter words (24 bits, set at reset)
     pa_sweep_trace_t* trace;   // [N][T] or null
     // patch-MLP weights in device layouts
     const __bf16* w1t;         // [hidden][16]     (transposed W1)

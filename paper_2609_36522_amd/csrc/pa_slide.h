@@ -26,6 +26,7 @@ struct SlideScratch {
     double dv[PA_MAX_WINDOW];       // deviations of states s+1..e-1 from their cache entries
     int wfirst[4], wbad[4], wcount[4], wrev[4], wbelow[4];
     int s2;                         // new window start
+    int nonfinite;                  // sticky non-finite flag after this slide (writer only)
     // results for the caller (valid after the call on every thread)
     int done, m, newest;
     int miss_idx[PA_MAX_WINDOW];    // ascending misses of the next window
@@ -68,6 +69,17 @@ __device__ void slide_partials(const Dev& d, int n, double* sub) {
         for (int b = u; b < nblk; b += kSlideSubs) acc += pr[b];
         sub[idx] = acc;
     }
+}
+
+// Progress word of sample n for the host's launch loop (pinned host memory, system scope):
+// completed sweeps << 32 | done << 31 | nonfinite << 30 | window start (at most T < 2^30).
+// The host reads the words, and the counter words of a done sample; anything else only after
+// synchronizing the stream.
+__device__ __forceinline__ void publish_progress(const Dev& d, int n, int sweeps, int done, int nonfinite,
+                                                 int s) {
+    const uint64_t word = ((uint64_t)(uint32_t)sweeps << 32) | ((uint64_t)(done ? 1 : 0) << 31) |
+                          ((uint64_t)(nonfinite ? 1 : 0) << 30) | (uint64_t)(uint32_t)s;
+    __hip_atomic_store(d.progress + n, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // Every thread of the block calls it (it synchronizes the block), after slide_partials into
@@ -134,17 +146,27 @@ __device__ void slide_core(const Dev& d, int n, const SlidePre& pre, bool writer
             ctrl->e = min(s2 + d.P, d.T);
             ctrl->done = s2 >= d.T;
             ctrl->sweep = pre.sweep + 1;
-            // Progress word for the host's launch loop (pinned host memory, system scope; the
-            // host only reads this word and synchronizes the stream before reading anything
-            // else).
-            const uint64_t word = ((uint64_t)(uint32_t)(pre.sweep + 1) << 32) |
-                                  ((uint64_t)(s2 >= d.T) << 31) | (uint64_t)(uint32_t)min(s2, d.T);
-            __hip_atomic_store(d.progress + n, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            sc.nonfinite = (pre.nonfinite || anybad) ? 1 : 0;
         }
     }
     __syncthreads();
     const int s2 = sc.s2;
-    if (s2 >= d.T) return;                  // uniform; no next window, counters unchanged
+    if (s2 >= d.T) {                        // uniform; no next window, counters unchanged
+        if (writer && tid == 0) {
+            // The sample is done: its final counters for the host (tagged with the sample's
+            // epoch, so that the host can tell them from an earlier sample's), then the word.
+            if (d.counters) {
+                const uint64_t tag = (uint64_t)(d.epoch & 0xffffffu) << 40;
+                const int64_t v[4] = {pre.nfe, pre.hits, pre.revisits, pre.revisits_below};
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    __hip_atomic_store(d.counters + 4 * n + k, tag | ((uint64_t)v[k] & ((1ull << 40) - 1)),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            }
+            publish_progress(d, n, pre.sweep + 1, 1, sc.nonfinite, d.T);
+        }
+        return;
+    }
 
     // Next window [s2, e2): Eq. (4)-(5) for slots that hold a cache entry (t < e); first
     // entries (t >= e) are misses; compaction by wave ballots and LDS offsets.
@@ -203,6 +225,7 @@ __device__ void slide_core(const Dev& d, int n, const SlidePre& pre, bool writer
                 ctrl->hits = pre.hits + (W2 - m);
                 ctrl->revisits = pre.revisits + sc.wrev[0] + sc.wrev[1] + sc.wrev[2] + sc.wrev[3];
                 ctrl->revisits_below = pre.revisits_below + sc.wbelow[0] + sc.wbelow[1] + sc.wbelow[2] + sc.wbelow[3];
+                publish_progress(d, n, pre.sweep + 1, 0, sc.nonfinite, s2);
             }
         }
     }

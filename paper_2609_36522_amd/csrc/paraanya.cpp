@@ -25,7 +25,8 @@ struct paraanya {
     int model = PA_EPS_LINEAR;
     std::vector<double> coef_host;    // [T][3] as uploaded
     Ctrl* ctrl_host = nullptr;        // pinned mirror, one block per sample
-    uint64_t* progress_host = nullptr; // pinned, device-mapped progress words (see k_slide)
+    uint64_t* progress_host = nullptr; // pinned, device-mapped: [N] progress words, then [N][4]
+                                       // final counter words (see publish_progress, slide_core)
     float* noise_buf = nullptr;       // [N][T][D] step noise (eta > 0)
     bool noise_set = false;
     bool ctrl_fresh = false;           // ctrl_host matches the device and nothing is queued
@@ -35,6 +36,9 @@ struct paraanya {
     pa::KernelTimer timer;            // kinds: 0 network, 1 Picard, 2 slide
     int64_t timed_latents = 0;        // network latents of the samples the timer covers
     bool slide_pending = false;       // fused sweep: the last sweep's slide is not computed yet
+    bool head_valid = false;          // ctrl_host's counters are final (taken from the counter
+                                      // words by paraanya_sample; work may still be queued)
+    bool progress_quiet = false;      // nothing queued can still write a progress word
 
     ~paraanya() {
         (void)hipStreamSynchronize(stream);
@@ -68,6 +72,39 @@ struct paraanya {
         return false;
     }
 
+    // Every sample is done (its progress word says so): fills the counters of ctrl_host from
+    // the done words and the final counter words the last slide wrote before them, if all of
+    // those carry this sample's epoch (else the caller reads the control blocks the
+    // synchronizing way). The words are written by the device with system-scope stores that
+    // may reach host memory in any order, hence the epoch tag on each.
+    bool take_final_counters() {
+        const volatile uint64_t* w = progress_host;
+        const volatile uint64_t* cw = progress_host + d.N;
+        const uint64_t tag = (uint64_t)(d.epoch & 0xffffffu);
+        uint64_t v[PA_MAX_BATCH][4];
+        for (int n = 0; n < d.N; ++n)
+            for (int k = 0; k < 4; ++k) {
+                v[n][k] = cw[4 * n + k];
+                if ((v[n][k] >> 40) != tag) return false;
+            }
+        for (int n = 0; n < d.N; ++n) {
+            const uint64_t p = w[n];
+            Ctrl& c = ctrl_host[n];
+            c.sweep = (int32_t)(p >> 32);
+            c.done = (int32_t)((p >> 31) & 1u);
+            c.nonfinite = (int32_t)((p >> 30) & 1u);
+            c.s = (int32_t)(p & 0x3fffffffu);
+            c.e = c.s + d.P < d.T ? c.s + d.P : d.T;
+            const uint64_t mask = (1ull << 40) - 1;
+            c.nfe = (int64_t)(v[n][0] & mask);
+            c.hits = (int64_t)(v[n][1] & mask);
+            c.revisits = (int64_t)(v[n][2] & mask);
+            c.revisits_below = (int64_t)(v[n][3] & mask);
+        }
+        head_valid = true;
+        return true;
+    }
+
     // Start/stop events of one timed launch of kernel kind k, or nulls when untimed. Samples
     // drain the pool when they end; a handle driven sweep by sweep drains it (after waiting
     // for the stream) once kMaxPendingPairs launches are pending.
@@ -89,6 +126,7 @@ struct paraanya {
         // Under PROFILE every timed launch carries its own start/stop events (no marker
         // packets between kernels).
         ctrl_fresh = false;
+        head_valid = false;
         hipEvent_t e0, e1;
         int rc;
         if (model == PA_EPS_PATCH_MLP) {
@@ -236,12 +274,15 @@ int paraanya_create(const int32_t latent_shape[4], int32_t T, const pa_schedule_
     hipError_t he = hipHostMalloc((void**)&h->ctrl_host, Nz * sizeof(Ctrl), hipHostMallocDefault);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostMalloc"));
     memset(h->ctrl_host, 0, Nz * sizeof(Ctrl));
-    he = hipHostMalloc((void**)&h->progress_host, Nz * sizeof(uint64_t) < 256 ? 256 : Nz * sizeof(uint64_t),
+    // Progress words [N], then the final counter words [N][4].
+    const size_t words = 5 * Nz;
+    he = hipHostMalloc((void**)&h->progress_host, words * sizeof(uint64_t) < 256 ? 256 : words * sizeof(uint64_t),
                        hipHostMallocMapped | hipHostMallocCoherent);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostMalloc(progress)"));
-    for (size_t n = 0; n < Nz; ++n) h->progress_host[n] = 0;
+    for (size_t i = 0; i < words; ++i) h->progress_host[i] = 0;
     he = hipHostGetDevicePointer((void**)&d.progress, h->progress_host, 0);
     if (he != hipSuccess) return bail(hip_fail(he, "hipHostGetDevicePointer"));
+    d.counters = d.progress + Nz;
     // The host vectors above die at return: wait for the uploads that read them.
     he = hipStreamSynchronize(h->stream);
     if (he != hipSuccess) return bail(hip_fail(he, "hipStreamSynchronize"));
@@ -253,10 +294,15 @@ int paraanya_reset(paraanya_t* h, const float* x_init) {
     pa::g_err.clear();
     if (!h || !x_init) return fail(PA_ERR_INVALID_ARG, "NULL argument");
     if (h->noise_buf && !h->noise_set) return fail(PA_ERR_STATE, "eta > 0: set the step noise first (paraanya_set_noise)");
-    // No kernel of this handle may still publish progress from an earlier sample.
-    PA_HIP(hipStreamSynchronize(h->stream));
+    // No kernel of this handle may still publish progress from an earlier sample. After a
+    // paraanya_sample that saw every sample done, none can (the slide that published done was
+    // the last writer; later queued sweeps leave at once), so the stream need not be drained.
+    if (!h->progress_quiet) PA_HIP(hipStreamSynchronize(h->stream));
+    h->progress_quiet = false;
     for (int n = 0; n < h->d.N; ++n) h->progress_host[n] = 0;
+    h->d.epoch = (h->d.epoch + 1) & 0xffffffu;    // counter words of this sample carry it
     h->ctrl_fresh = false;
+    h->head_valid = false;
     const size_t row = (size_t)h->d.D * sizeof(float);
     PA_HIP(hipMemcpy2DAsync(h->d.X, (size_t)(h->d.T + 1) * row, x_init, row, row, (size_t)h->d.N,
                             hipMemcpyDeviceToDevice, h->stream));
@@ -323,7 +369,7 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
         *need = 0;
         for (int n = 0; n < N; ++n) {
             const uint64_t w = prog[n];
-            const int c = (int)(w >> 32), s_now = (int)(w & 0x7fffffffu);
+            const int c = (int)(w >> 32), s_now = (int)(w & 0x3fffffffu);
             if (c > *completed) *completed = c;
             if ((w >> 31) & 1u) continue;
             all = false;
@@ -359,18 +405,26 @@ int paraanya_sample(paraanya_t* h, const float* x_init, float* x_out) {
         }
     }
     // Every sample is done: the slide that published that also wrote the control block, so no
-    // finishing slide is needed. One synchronization for the output copy and the counters.
+    // finishing slide is needed. The output copy is queued behind the sample's last kernels.
     h->slide_pending = false;
     const size_t row = (size_t)h->d.D * sizeof(float);
     PA_HIP(hipMemcpy2DAsync(x_out, row, h->d.X + (size_t)T * h->d.D, (size_t)(T + 1) * row, row,
                             (size_t)N, hipMemcpyDeviceToDevice, h->stream));
     h->ctrl_fresh = false;
-    if ((rc = h->read_ctrl())) return rc;
-    for (int n = 0; n < N; ++n) h->timed_latents += h->ctrl_host[n].nfe;
-    // The stream is idle (read_ctrl synchronized it): fold this sample's event pairs into the
-    // running totals, so the pool stays at one sample's launches.
-    if (h->flags & PA_FLAG_PROFILE)
-        if ((rc = h->timer.drain())) return rc;
+    h->host_done = true;
+    if (!(h->flags & PA_FLAG_PROFILE) && h->take_final_counters()) {
+        // No synchronization: the counters came with the done words, and what is still queued
+        // (the tail of the last kernels, the copy) is ordered before the caller's next work on
+        // the stream.
+        h->progress_quiet = true;
+    } else {
+        if ((rc = h->read_ctrl())) return rc;
+        for (int n = 0; n < N; ++n) h->timed_latents += h->ctrl_host[n].nfe;
+        // The stream is idle (read_ctrl synchronized it): fold this sample's event pairs into
+        // the running totals, so the pool stays at one sample's launches.
+        if (h->flags & PA_FLAG_PROFILE)
+            if ((rc = h->timer.drain())) return rc;
+    }
     if (h->any_nonfinite()) return fail(PA_ERR_NONFINITE, "non-finite residual during sampling");
     return PA_OK;
 }
@@ -396,7 +450,7 @@ int paraanya_stats(paraanya_t* h, pa_stats_t* out) {
     pa::g_err.clear();
     if (!h || !out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
     if (!h->have_reset) return fail(PA_ERR_STATE, "stats before reset");
-    int rc = h->read_ctrl();
+    int rc = h->head_valid ? PA_OK : h->read_ctrl();
     if (rc) return rc;
     fill_stats(h->ctrl_host[0], out);
     for (int n = 1; n < h->d.N; ++n) {
@@ -421,7 +475,7 @@ int paraanya_stats_sample(paraanya_t* h, int32_t n, pa_stats_t* out) {
     if (!h || !out) return fail(PA_ERR_INVALID_ARG, "NULL argument");
     if (n < 0 || n >= h->d.N) return fail(PA_ERR_INVALID_ARG, "sample %d outside [0, %d)", n, h->d.N);
     if (!h->have_reset) return fail(PA_ERR_STATE, "stats before reset");
-    int rc = h->read_ctrl();
+    int rc = h->head_valid ? PA_OK : h->read_ctrl();
     if (rc) return rc;
     fill_stats(h->ctrl_host[n], out);
     return PA_OK;
@@ -602,7 +656,7 @@ int paraanya_sample_noalloc(const int32_t latent_shape[4], int32_t T, const pa_s
         for (size_t n = 0; n < Nz; ++n) {
             if ((words[n] >> 31) & 1u) continue;
             all = false;
-            const int s_now = (int)(words[n] & 0x7fffffffu);
+            const int s_now = (int)(words[n] & 0x3fffffffu);
             const int qn = (T - s_now + q.P - 1) / q.P;
             if (qn > need) need = qn;
         }

@@ -385,3 +385,32 @@ def test_largest_handle_offsets(gpu_lib):
         ref = net.eval_one(Xh[i], t)
         assert H.eps_error(Eh[i], ref, shape) <= H.EPS_RTOL, t
     assert np.isfinite(out).all() and not np.array_equal(out[0], out[N - 1])
+
+
+@pytest.mark.parametrize("wl,batch", [(W.TINY_LINEAR, 3), (W.SMALL_MLP, 1), (W.SD_MLP, 1), (W.SMALL_MLP, 2)],
+                         ids=["linear_batch3", "mlp_small", "mlp_sd", "mlp_small_batch2"])
+def test_sample_counters_from_done_words(wl, batch, gpu_lib):
+    """paraanya_sample returns once every sample's done word is seen, without draining the
+    stream, and takes the counters from the final counter words the last slide wrote (tagged
+    with the sample's epoch). They must equal what the control blocks hold after a full
+    synchronization (a profiling handle always takes that path), sample by sample, over
+    several samples in a row on one handle; the outputs, read after the stream, must agree
+    bit for bit, and a reset right after a sample must not see the previous sample's words."""
+    xb = inputs.x_init_batch(wl.latent, batch).reshape(-1) if batch > 1 else inputs.x_init(wl.latent).reshape(-1)
+    x = torch.from_numpy(xb).cuda()
+    runs = []
+    for profile in (False, True):
+        with B.from_workload(wl, batch=batch, profile=profile) as s:
+            got = []
+            for _ in range(3):
+                out = s.sample(x)
+                st = [s.stats()] + [s.stats(n) for n in range(batch)]
+                got.append((out.cpu().numpy(), st))
+            s.reset(x)                       # the next sample starts from a clean slate
+            s.sweep(sync=True)
+            assert s.stats()["sweeps"] == 1
+        runs.append(got)
+    for (o0, s0), (o1, s1) in zip(*runs):
+        assert np.array_equal(o0, o1)
+        assert s0 == s1, (s0, s1)
+    assert runs[0][0][1] == runs[0][2][1]    # the same input gives the same counters each time
