@@ -288,6 +288,8 @@ class Sampler:
         return bool(done.value)
 
     def sample(self, x_init, x_out=None):
+        """paraanya_sample: returns once every sample is done; x_out is written by work queued
+        on the handle's stream (torch operations on that stream see it)."""
         if x_out is None:
             x_out = self.torch.empty_like(x_init)
         _check(self.lib.paraanya_sample(self.h, self._dev(x_init), self._dev(x_out)))
