@@ -414,3 +414,22 @@ def test_sample_counters_from_done_words(wl, batch, gpu_lib):
         assert np.array_equal(o0, o1)
         assert s0 == s1, (s0, s1)
     assert runs[0][0][1] == runs[0][2][1]    # the same input gives the same counters each time
+
+
+@pytest.mark.parametrize("wl", [W.TINY_LINEAR, W.SMALL_MLP], ids=["linear", "mlp"])
+def test_chained_samples_are_stream_ordered(wl, gpu_lib):
+    """paraanya_sample returns before its output copy has run; feeding each output straight
+    back as the next sample's input (no synchronization in between, in place and into a second
+    tensor) must give what a synchronizing handle gives."""
+    x = _x(wl)
+    results = []
+    for profile in (False, True):
+        with B.from_workload(wl, profile=profile) as s:
+            a = x.clone()
+            b = torch.empty_like(a)
+            s.sample(a, b)          # b <- sample(x)
+            s.sample(b, b)          # in place
+            s.sample(b, a)          # a <- sample(b)
+            results.append(a.cpu().numpy())
+    assert np.array_equal(results[0], results[1])
+    assert np.isfinite(results[0]).all()
