@@ -53,7 +53,7 @@ CASES = [
     ("mlp_small", W.SMALL_MLP, 0.05, dict(independent=True)),
     ("mlp_small_delta0", W.SMALL_MLP, 0.0, dict(independent=True)),
     ("mlp_sd", W.SD_MLP, 0.05, dict(independent=True)),
-    ("mlp_sd_delta0", W.SD_MLP, 0.0),
+    ("mlp_sd_delta0", W.SD_MLP, 0.0, dict(independent=True)),
     # the rest of the headline delta sweep
     ("mlp_sd_delta002", W.SD_MLP, 0.02, dict(eps_stride=4)),
     ("mlp_sd_delta01", W.SD_MLP, 0.1, dict(eps_stride=4)),
