@@ -8,7 +8,8 @@ multiple of 4, 1..5 x 1..20 x 1..20, T up to 300) or patch-MLP (hidden 512, 1024
 samples per handle, eta in {0, 0.5, 1}. Each run is checked as in test_gpu_parity.py: every
 sweep step-locked against the oracle (decisions exactly, states within one fp32 ulp),
 counters consistent with the traces, network outputs against the oracle network, and the
-followed final latent within 1e-4 x RMS.
+followed final latent within 1e-4 x RMS. Then 12 seeded random configurations of the
+Parareal sampler, checked as in test_gpu_parareal.py.
 """
 import math
 import random
@@ -77,3 +78,36 @@ def test_random_configuration(wl, batch, eta, gpu_lib):
               flush=True)
     finally:
         run.close()
+
+
+def _parareal_configs():
+    import test_gpu_parareal as TP
+    rng = random.Random(SEED + 1)
+    out = []
+    for i in range(12):
+        mlp = rng.random() < 0.4
+        B = rng.randint(1, 12)
+        T = B * rng.randint(1, 10)
+        if mlp:
+            hw = rng.choice([(16, 32), (32, 32), (32, 64), (48, 64), (32, 96)])
+            wl = TP._wl(f"pr_rand{i}", (4, hw[0], hw[1]), T, B, "patch_mlp", rng.choice([512, 1024, 2048]))
+        else:
+            while True:
+                lat = (rng.randint(1, 5), rng.randint(1, 16), rng.randint(1, 16))
+                if (lat[0] * lat[1] * lat[2]) % 4 == 0:
+                    break
+            wl = TP._wl(f"pr_rand{i}", lat, T, B)
+        out.append((wl, rng.choice([0.0, 0.01, 0.05, 0.2, INF])))
+    return out
+
+
+PR_CONFIGS = _parareal_configs()
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("wl,delta", PR_CONFIGS, ids=[c[0].name for c in PR_CONFIGS])
+def test_random_parareal_configuration(wl, delta, gpu_lib):
+    """The Parareal sampler on 12 seeded random configurations (1 to 12 blocks of 1 to 10 fine
+    steps; linear or patch-MLP), checked as in test_gpu_parareal.py."""
+    import test_gpu_parareal as TP
+    TP.test_parareal_parity(wl.name, wl, delta, gpu_lib)
