@@ -55,3 +55,41 @@ def test_noalloc_in_place_and_limits(gpu_lib):
     assert ei.value.code == B.PA_ERR_INVALID_ARG and "workspace" in str(ei.value)
     out, st = B.sample_noalloc_workload(wl, x)                # still works after the refusal
     assert np.array_equal(out.cpu().numpy(), ref) and st == st_ref
+
+
+def test_noalloc_random_configurations(gpu_lib):
+    """Ten seeded random deterministic-step configurations (linear or patch-MLP, ragged linear
+    latents, any window, delta and tau, 1 to 5 samples): the allocation-free call equals the
+    handle path bit for bit, or, if its buffers do not fit the workspace, refuses with
+    PA_ERR_INVALID_ARG and leaves the next call working."""
+    import math
+    import random
+    from paper_2609_36522_amd.workloads import Workload
+    rng = random.Random(20260202)
+    ran = 0
+    for i in range(10):
+        if rng.random() < 0.4:
+            hw = rng.choice([(16, 32), (32, 32), (32, 64), (48, 64)])
+            wl = Workload(f"na_rand{i}", (4, hw[0], hw[1]), rng.randint(2, 60), 1, 0.05, 1e-3, "patch_mlp",
+                          hidden=rng.choice([512, 1024]))
+        else:
+            while True:
+                lat = (rng.randint(1, 5), rng.randint(1, 20), rng.randint(1, 20))
+                if (lat[0] * lat[1] * lat[2]) % 4 == 0:
+                    break
+            wl = Workload(f"na_rand{i}", lat, rng.randint(1, 300), 1, 0.05, 1e-3, "linear")
+        wl = wl.with_(window=rng.randint(1, min(wl.T, 256)), delta=rng.choice([0.0, 0.05, 0.3, math.inf]),
+                      tol=rng.choice([0.0, 1e-3, 1e-1]))
+        n = rng.choice([1, 1, 2, 5])
+        x = _x(wl, n)
+        print(f"[noalloc] {wl.name}: {wl.model} latent={wl.latent} T={wl.T} P={wl.window} "
+              f"delta={wl.delta} tol={wl.tol} batch={n}", flush=True)
+        ref, st_ref = _reference(wl, x, n)
+        try:
+            out, st = B.sample_noalloc_workload(wl, x, batch=n)
+        except B.PAError as e:
+            assert e.code == B.PA_ERR_INVALID_ARG and "workspace" in str(e), str(e)
+            continue
+        ran += 1
+        assert np.array_equal(out.cpu().numpy(), ref) and st == st_ref, wl.name
+    assert ran >= 5
