@@ -8,8 +8,8 @@ Two checks per workload, both through the C ABI (binding.Sampler):
   rows. For the patch-MLP the oracle consumes the device's fresh outputs for the misses
   ("eps-locked"), and those outputs are checked separately against the oracle network.
 * follow: the oracle runs its own trajectory from the same initial latent (fully independent
-  for the linear network; eps-locked for the patch-MLP) and must reproduce every decision
-  and the final latent within 1e-4 x RMS.
+  for the linear network; eps-locked for the patch-MLP), advanced sweep by sweep beside the
+  device run, and must reproduce every decision and the final latent within 1e-4 x RMS.
 
 Decision rule: the device decides in fp32, the oracle in fp64. A decision may differ only if
 the oracle's deviation lies within BAND (relative) of delta, or the deciding residual within
@@ -31,7 +31,12 @@ from paper_2609_36522_amd import binding, inputs
 # deviation or residual by a few fp64 ulps of the sum.
 BAND = 1e-6                 # relative decision band around delta and tau (logged, not failed)
 STATE_ULPS = 1              # per-sweep updated states, in fp32 ulps of the oracle value
-STATE_FRAC = 1e-4           # at most this fraction of state elements may differ at all
+# At most max(1, STATE_FRAC x n) of the n state elements a sweep updates may differ at all. A
+# tie needs the fp64 sum within a few fp64 ulps of an fp32 rounding midpoint, which happened
+# once in about 1e7 updated elements over hundreds of random configurations; one tie in a
+# sweep of a tiny latent (80 elements, 51 states) is that event, while a systematic change of
+# the arithmetic (an fp32 partial sum, a dropped term) moves many elements at once.
+STATE_FRAC = 1e-4
 FINAL_RTOL = 1e-4           # final latent, max-abs x RMS
 SUM_RTOL = 1e-11            # deviations/residuals: fp64 sums in different orders
 # Fresh network outputs: max-abs error <= EPS_RTOL x the larger of the output's RMS over the
@@ -46,10 +51,10 @@ SUM_RTOL = 1e-11            # deviations/residuals: fp64 sums in different order
 EPS_RTOL = 1e-2
 REVISIT_THR = 0.05          # default threshold of the device's revisit counters
 # An oracle trajectory of its own (follow) stores its own fp32 states, which may differ from
-# the device's by one rounding in a few elements (the step-locked check allows that); an
-# Eq. (4) deviation, a mean of |x - x^| over D entries, then moves by (1/D) sum |diff|, a few
-# 1e-9 relative. Deviations of a followed trajectory must agree within the decision band.
-FOLLOW_DEV_RTOL = BAND
+# the device's by a rounding in a few elements, then by what the dynamics make of it. For
+# every cached slot the harness measures, before the sweep, a = mean |x_o - x_d| +
+# mean |x^_o - x^_d| over the D entries; by the triangle inequality the two Eq. (4)
+# deviations, means of |x - x^|, differ by at most a, plus the fp64 sum order (SUM_RTOL).
 
 
 def coefficients(T, eta=0.0):
@@ -86,14 +91,16 @@ class Log:
         self.flips.append((kind, sweep, slot, float(value), float(threshold)))
 
 
-def _in_band(v, thr) -> bool:
-    return abs(v - thr) <= BAND * max(abs(thr), 1e-30)
+def _in_band(v, thr, extra=0.0) -> bool:
+    """v within BAND (relative) of the threshold, widened by ``extra`` (follow: how far the
+    two sides' states can move v)."""
+    return abs(v - thr) <= BAND * max(abs(thr), 1e-30) + extra
 
 
-def _check_hits(k, dev_o, gpu, delta, log, rtol=SUM_RTOL):
+def _check_hits(k, dev_o, gpu, delta, log, allow=None):
     """Compare the oracle's deviations/hits (fp64) with the device's; returns the mask to use.
-    ``rtol``: SUM_RTOL when both sides hold the same fp32 states (step-locked); FOLLOW_DEV_RTOL
-    when the oracle follows its own trajectory."""
+    ``allow`` (follow only): per window slot, how far the two sides' states can move the
+    deviation (mean |x_o - x_d| + mean |x^_o - x^_d|); step-locked, both hold the same states."""
     W = len(dev_o)
     assert gpu["e"] - gpu["s"] == W
     dev_g = gpu["dev"]
@@ -101,11 +108,17 @@ def _check_hits(k, dev_o, gpu, delta, log, rtol=SUM_RTOL):
     ok = ~np.isnan(dev_o)
     if ok.any():
         err = np.abs(dev_g[ok] - dev_o[ok])
-        assert np.all(err <= rtol * dev_o[ok] + 1e-300), f"sweep {k}: deviation mismatch {err.max()}"
+        bound = SUM_RTOL * np.maximum(dev_o[ok], dev_g[ok])
+        if allow is not None:
+            bound = bound + (1.0 + SUM_RTOL) * allow[ok]
+        j = int(np.argmax(err - bound))
+        assert np.all(err <= bound + 1e-300), \
+            f"sweep {k}: deviation mismatch {err[j]!r} (oracle {dev_o[ok][j]!r}, bound {bound[j]!r})"
     hit_o = ok & (np.nan_to_num(dev_o, nan=np.inf) < delta)
     hit_g = gpu["hit"]
     for j in np.nonzero(hit_o != hit_g)[0]:
-        assert _in_band(dev_o[j], delta), f"sweep {k} slot {j}: hit decision differs outside the band " \
+        extra = 0.0 if allow is None else (1.0 + SUM_RTOL) * allow[j]
+        assert _in_band(dev_o[j], delta, extra), f"sweep {k} slot {j}: hit decision differs outside the band " \
                                           f"(dev {dev_o[j]!r}, delta {delta!r})"
         log.flip("hit", k, int(j), dev_o[j], delta)
     return hit_g.copy()
@@ -133,7 +146,7 @@ class Run:
     inputs.x_init_batch) and checks every sample that is still running after each batched
     sweep. ``eta`` > 0 runs the stochastic step with the seeded step noise."""
 
-    def __init__(self, wl, delta, *, eps_stride=1, seed_x=inputs.SEED_X_INIT, keep_eps=True,
+    def __init__(self, wl, delta, *, eps_stride=1, seed_x=inputs.SEED_X_INIT,
                  x_init=None, batch=1, eta=0.0):
         import torch
         self.wl, self.delta = wl, float(delta)
@@ -155,12 +168,14 @@ class Run:
             self.noise = [sp.step_noise_terms(self.sigma, self.Z[n]) for n in range(self.N)]
         self.log = Log()
         self.records = [[] for _ in range(self.N)]    # device trace records per sample
-        self.eps_rows = [[] for _ in range(self.N)]   # per sample, per sweep {t: fresh output}
+        # follow: the oracle's own trajectory per sample, its decision log and trace
+        self.fol = [sp.init_state(self.xs[n], self.T) for n in range(self.N)]
+        self.follow_logs = [Log() for _ in range(self.N)]
+        self.follow_traces = [[] for _ in range(self.N)]
         # Fresh network outputs checked one by one against the oracle network: every output
         # of the first sweep, then every eps_stride-th fresh output of the run (counted over
         # all samples in sweep order); eps_stride = 1 checks every output, 0 none.
         self.eps_stride = int(eps_stride)
-        self.keep_eps = keep_eps
         self.eps_err = []          # max-abs/RMS of every checked fresh output
         self._eps_seen = 0
         self.state_diffs = 0       # updated state elements that differ (by one ulp) at all
@@ -197,11 +212,12 @@ class Run:
                 o.valid[:] = False
                 o.valid[sw:c1] = vg
                 o.s, o.newest = sw, newest[n]
-                pre[n] = (sw, e)
+                pre[n] = (sw, e, self._follow_allowance(n, k, sw, e, Xg, Xhg, c1))
             s.sweep(sync=True)
             for n in active:
-                sw, e = pre[n]
-                self._check_sweep(n, k, sw, e, ost[n], newest[n])
+                sw, e, allow = pre[n]
+                g, gpu_eps = self._check_sweep(n, k, sw, e, ost[n], newest[n])
+                self._follow_sweep(n, k, g, gpu_eps, allow)
                 newest[n] = max(newest[n], e)
             k += 1
             assert k <= T, "more sweeps than steps"
@@ -238,8 +254,9 @@ class Run:
         diff = np.abs(Xp[1:].astype(np.float64) - ref.astype(np.float64))
         ulp = np.spacing(np.abs(ref)).astype(np.float64)
         assert np.all(diff <= STATE_ULPS * ulp), f"sample {n} sweep {k}: states differ by {np.max(diff / ulp):.3g} ulp"
-        assert np.mean(diff > 0) <= STATE_FRAC, f"sample {n} sweep {k}: {np.mean(diff > 0):.3g} of states differ"
-        self.state_diffs += int(np.count_nonzero(diff))
+        nd = int(np.count_nonzero(diff))
+        assert nd <= max(1, STATE_FRAC * diff.size), f"sample {n} sweep {k}: {nd} of {diff.size} state elements differ"
+        self.state_diffs += nd
         _check_slide(k, rec["r"], g, self.wl.tol, self.log, float(diff.max(initial=0.0)))
         # cache: inputs of the misses are the pre-update states, hits untouched
         for j in range(e - sw):
@@ -263,40 +280,54 @@ class Run:
                 self.eps_err.append(e_rel)
                 assert e_rel <= EPS_RTOL, f"sample {n} sweep {k}: network output of {t} off by {e_rel:.3g} x its scale"
         self.records[n].append(g)
-        if self.keep_eps and self.wl.model != "linear":
-            self.eps_rows[n].append(gpu_eps)
+        return g, gpu_eps
+
+    def _follow_allowance(self, n, k, sw, e, Xg, Xhg, c1):
+        """Before device sweep k: bring the followed trajectory of sample n to the same window
+        and measure, per cached slot, mean |x_o - x_d| + mean |x^_o - x^_d| against the
+        device's pre-state rows (Xg from state sw, Xhg for sw..c1-1)."""
+        f = self.fol[n]
+        assert f.s == sw, f"follow sweep {k}: window start {f.s} vs {sw}"
+        sp.fill_new_states(f.X, f.newest, e)
+        allow = np.zeros(e - sw)
+        for j in range(e - sw):
+            t = sw + j
+            if t < c1 and f.valid[t]:
+                allow[j] = (np.abs(f.X[t].astype(np.float64) - Xg[j]).mean()
+                            + np.abs(f.Xh[t].astype(np.float64) - Xhg[j]).mean())
+        return allow
+
+    def _follow_sweep(self, n, k, g, gpu_eps, allow):
+        """Sweep k of the followed trajectory of sample n, after the device's: its own states,
+        the device's decisions within the band, and for the patch-MLP the device's fresh outputs."""
+        f, log = self.fol[n], self.follow_logs[n]
+        e = sp.window_end(f.s, self.T, self.P)
+        dev_o, _ = sp.cache_test(f.X, f.Xh, f.valid, f.s, e, self.delta)
+        hit = _check_hits(k, dev_o, g, self.delta, log, allow=allow)
+        if self.wl.model == "linear":
+            eps_fn = self.net
+        else:
+            def eps_fn(Xb, steps, _r=gpu_eps):
+                assert list(steps) == list(_r.keys())
+                return np.stack([_r[t] for t in steps]).astype(Xb.dtype)
+        noise = None if self.noise is None else self.noise[n]
+        rec = sp.sweep(f, self.P, self.delta, self.wl.tol, self.alpha, self.b, eps_fn,
+                       force_hit=hit, noise=noise)
+        rec["allow"] = allow
+        self.follow_traces[n].append(rec)
+        assert rec["miss"] == g["miss"]
+        if rec["c"] != g["c"]:
+            j = min(rec["c"], g["c"])
+            assert _in_band(rec["r"][j], self.wl.tol), f"follow sweep {k}: slide differs"
+            log.flip("tau", k, j, rec["r"][j], self.wl.tol)
+            f.s = g["s_next"]
 
     def follow(self, n=0):
-        """Oracle trajectory of its own for sample n (eps-locked for the patch-MLP); returns
-        the x_T error / RMS. Also checks the device's revisit counters against the oracle's."""
-        T, P = self.T, self.P
-        st = sp.init_state(self.xs[n], T)
-        noise = None if self.noise is None else self.noise[n]
-        log = Log()
-        trace = []
-        for k, g in enumerate(self.records[n]):
-            assert st.s == g["s"], f"follow sweep {k}: window start {st.s} vs {g['s']}"
-            e = sp.window_end(st.s, T, P)
-            sp.fill_new_states(st.X, st.newest, e)
-            dev_o, _ = sp.cache_test(st.X, st.Xh, st.valid, st.s, e, self.delta)
-            hit = _check_hits(k, dev_o, g, self.delta, log, rtol=FOLLOW_DEV_RTOL)
-            if self.wl.model == "linear":
-                eps_fn = self.net
-            else:
-                rows = self.eps_rows[n][k]
-                def eps_fn(Xb, steps, _r=rows):
-                    assert list(steps) == list(_r.keys())
-                    return np.stack([_r[t] for t in steps]).astype(Xb.dtype)
-            rec = sp.sweep(st, P, self.delta, self.wl.tol, self.alpha, self.b, eps_fn,
-                           force_hit=hit, noise=noise)
-            trace.append(rec)
-            assert rec["miss"] == g["miss"]
-            c_o = rec["c"]
-            if c_o != g["c"]:
-                j = min(c_o, g["c"])
-                assert _in_band(rec["r"][j], self.wl.tol), f"follow sweep {k}: slide differs"
-                log.flip("tau", k, j, rec["r"][j], self.wl.tol)
-                st.s = g["s_next"]
+        """The followed trajectory of sample n (advanced during run()): its counters, revisit
+        counters and final latent against the device's; returns the x_T error / RMS."""
+        T = self.T
+        st, trace, log = self.fol[n], self.follow_traces[n], self.follow_logs[n]
+        assert len(trace) == len(self.records[n])
         stn = self.stats_n[n]
         assert st.done and st.nfe == stn["nfe"] and st.hits == stn["hits"]
         # revisit counters (default threshold 0.05): the oracle's count from its own trace;
@@ -304,7 +335,7 @@ class Run:
         req, rev, below = sp.revisit_counts(trace, REVISIT_THR)
         assert req == stn["nfe"] + stn["hits"] and rev == stn["revisits"]
         near = sum(int(np.count_nonzero(np.abs(np.nan_to_num(np.asarray(r["dev"]), nan=-1.0) - REVISIT_THR)
-                                        <= BAND * REVISIT_THR)) for r in trace)
+                                        <= BAND * REVISIT_THR + (1.0 + SUM_RTOL) * r["allow"])) for r in trace)
         assert abs(below - stn["revisits_below"]) <= near, (below, stn["revisits_below"])
         ref = st.X[T].astype(np.float64)
         x_T = self.x_T_all[n]
