@@ -54,7 +54,12 @@ __device__ __forceinline__ SlidePre slide_pre_of(const Ctrl& c) {
 // the partials u, u + kSlideSubs, ... in order. The order does not depend on the block size,
 // so every caller (k_slide, the fused network kernel) obtains the same fp64 values bit for
 // bit; the loads of a sub-sum are independent. Slots beyond the window hold stale partials,
-// summed and never used. The caller synchronizes the block before slide_core.
+// summed and never used. The caller synchronizes the block before slide_core. A thread issues
+// the loads of kSlideBatch partials of a sub-sum at once (one base address, constant offsets),
+// then adds them in order: one round trip to L2 per 32 partials instead of one per few loads;
+// the partials after the last whole batch follow one by one, in the same order.
+constexpr int kSlideBatch = 32;
+
 template <int NT>
 __device__ void slide_partials(const Dev& d, int n, double* sub) {
     const int tid = threadIdx.x;
@@ -65,8 +70,15 @@ __device__ void slide_partials(const Dev& d, int n, double* sub) {
         const double* pr = (q < P) ? d.part_res + pbase + (size_t)q * nblk
                                    : d.part_dev + pbase + (size_t)(q - P) * nblk;
         double acc = 0.0;
-#pragma unroll 8
-        for (int b = u; b < nblk; b += kSlideSubs) acc += pr[b];
+        int b = u;
+        for (; b + (kSlideBatch - 1) * kSlideSubs < nblk; b += kSlideBatch * kSlideSubs) {
+            double v[kSlideBatch];
+#pragma unroll
+            for (int i = 0; i < kSlideBatch; ++i) v[i] = pr[b + i * kSlideSubs];
+#pragma unroll
+            for (int i = 0; i < kSlideBatch; ++i) acc += v[i];
+        }
+        for (; b < nblk; b += kSlideSubs) acc += pr[b];
         sub[idx] = acc;
     }
 }
