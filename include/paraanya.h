@@ -71,7 +71,9 @@ extern "C" {
  * time embedding of the patch-MLP). Copied at create.
  * eta in [0, 1] selects the step (the generalized DDIM step of the DDIM paper):
  * x_{i+1} = sqrt(ab_{i+1}) x0^ + sqrt(1 - ab_{i+1} - sigma_i^2) eps + sigma_i z_i with
- * sigma_i = eta sqrt((1 - ab_{i+1}) / (1 - ab_i)) sqrt(1 - ab_i / ab_{i+1}). eta = 0 is
+ * sigma_i = eta sqrt((1 - ab_{i+1}) / (1 - ab_i)) sqrt(1 - ab_i / ab_{i+1}), taken as 0 at
+ * eta = 0 and where ab_{i+1} = ab_i (a step with no noise; with eta > 0 alpha_bar must not
+ * decrease, else PA_ERR_INVALID_ARG). eta = 0 is
  * deterministic DDIM; eta = 1 is ancestral DDPM sampling (the stochastic sampler of the
  * paper's window study, Sec. 3.4), whose per-step noise z_i is drawn before sampling and
  * given with paraanya_set_noise, so that Picard iteration solves a fixed recurrence. */

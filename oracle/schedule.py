@@ -68,7 +68,13 @@ def step_coefficients(ab: np.ndarray, eta: float):
     increment d_i = alpha_i x_i + b_i eps_i + sigma_i z_i (eta = 0 gives ddim_coefficients)."""
     ab = np.asarray(ab, dtype=np.float64)
     ab0, ab1 = ab[:-1], ab[1:]
-    sigma = eta * np.sqrt((1.0 - ab1) / (1.0 - ab0)) * np.sqrt(1.0 - ab0 / ab1)
+    # sigma_i is eta times the two factors: 0 at eta = 0 by definition, and 0 where
+    # ab_{i+1} = ab_i (the second factor is 0, the first at most 1), also where both are 1
+    # and the first factor is 0/0.
+    noiseless = (ab1 == ab0) | (eta == 0.0)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        full = eta * np.sqrt((1.0 - ab1) / (1.0 - ab0)) * np.sqrt(1.0 - ab0 / ab1)
+    sigma = np.where(noiseless, 0.0, full)
     a = np.sqrt(ab1 / ab0)
     alpha = a - 1.0
     x0_coef_eps = np.sqrt(1.0 - ab1 - sigma * sigma)

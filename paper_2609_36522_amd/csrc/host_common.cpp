@@ -69,6 +69,12 @@ int build_schedule(const pa_schedule_t* sc, int T, double* ab, double* tv) {
         return fail(PA_ERR_INVALID_ARG, "schedule: unknown kind %d", sc->kind);
     }
     if (!(sc->eta >= 0.0 && sc->eta <= 1.0)) return fail(PA_ERR_INVALID_ARG, "schedule: eta must lie in [0, 1] (got %g)", sc->eta);
+    if (sc->eta > 0.0) {
+        // The noise scale sigma_i needs ab_i <= ab_{i+1} (no real square root otherwise).
+        for (int i = 0; i < T; ++i)
+            if (!(ab[i + 1] >= ab[i]))
+                return fail(PA_ERR_INVALID_ARG, "schedule: alpha_bar must not decrease when eta > 0 (state %d)", i + 1);
+    }
     return PA_OK;
 }
 
@@ -80,10 +86,14 @@ int build_schedule(const pa_schedule_t* sc, int T, std::vector<double>& ab, std:
 
 void step_coefficients(const double* ab, int T, double eta, double* coef) {
     // One-step increment d_i = alpha_i x_i + b_i eps_i + sigma_i z_i of the generalized DDIM
-    // step with eta (eta = 0: DDIM; eta = 1: ancestral DDPM).
+    // step with eta (eta = 0: DDIM; eta = 1: ancestral DDPM). sigma_i is 0 at eta = 0, and
+    // where ab_{i+1} = ab_i (its second factor is 0 and its first at most 1; for
+    // ab_i = ab_{i+1} = 1 the first is 0/0), so a degenerate step has no NaN coefficients.
     for (int i = 0; i < T; ++i) {
         const double a = sqrt(ab[i + 1] / ab[i]);
-        const double sig = eta * sqrt((1.0 - ab[i + 1]) / (1.0 - ab[i])) * sqrt(1.0 - ab[i] / ab[i + 1]);
+        const double sig = (eta == 0.0 || ab[i + 1] == ab[i])
+                               ? 0.0
+                               : eta * sqrt((1.0 - ab[i + 1]) / (1.0 - ab[i])) * sqrt(1.0 - ab[i] / ab[i + 1]);
         coef[3 * i] = a - 1.0;
         coef[3 * i + 1] = sqrt(1.0 - ab[i + 1] - sig * sig) - a * sqrt(1.0 - ab[i]);
         coef[3 * i + 2] = sig;

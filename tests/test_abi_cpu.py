@@ -104,6 +104,17 @@ def test_explicit_schedule_validation():
     assert rc == B.PA_ERR_INVALID_ARG and "alpha_bar[2]" in msg
 
 
+def test_explicit_schedule_must_not_decrease_with_noise():
+    """With eta > 0 the noise scale needs ab_i <= ab_{i+1}: a decreasing explicit schedule is
+    refused at create (with eta = 0 the DDIM step is defined for it)."""
+    ab = np.array([0.5, 0.4, 1.0], np.float64)
+    tv = np.array([10, 5], np.int32)
+    sc = B.Schedule(B.PA_SCHED_EXPLICIT, 0, 0, 0, 0, 0, ab.ctypes.data_as(C.POINTER(C.c_double)),
+                    tv.ctypes.data_as(C.POINTER(C.c_int32)), 1.0)
+    rc, h, msg = _create(T=2, window=2, sched=sc)
+    assert rc == B.PA_ERR_INVALID_ARG and h is None and "must not decrease" in msg
+
+
 def test_null_handle_calls_fail_cleanly():
     lib = B.load_library()
     assert lib.paraanya_reset(None, None) == B.PA_ERR_INVALID_ARG

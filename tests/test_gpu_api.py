@@ -100,6 +100,28 @@ def test_explicit_schedule_matches_scaled_linear(gpu_lib):
         assert np.array_equal(s1.sample(x).cpu().numpy(), s2.sample(x).cpu().numpy())
 
 
+@pytest.mark.parametrize("eta", [0.0, 1.0])
+@pytest.mark.parametrize("delta", [0.0, 0.05])
+def test_identity_steps_converge_in_one_sweep_per_window(delta, eta, gpu_lib):
+    """alpha_bar = 1 at every state: every step is the identity (alpha = b = sigma = 0 in the
+    uploaded tables, no NaN), every Eq. (2) residual is exactly 0, and at tau = 0 (r <= tau)
+    each sweep slides the window to its end: ceil(T / P) sweeps, every step evaluated once,
+    the initial latent returned bit for bit."""
+    T, P = 12, 5
+    wl = W.TINY_LINEAR.with_(T=T, window=P, tol=0.0)
+    sched = {"alpha_bar": np.ones(T + 1), "t_values": sch.trailing_timesteps(T)}
+    x = _x(wl)
+    with B.from_workload(wl, delta, schedule=sched, eta=eta) as s:
+        a, b, sig, _ = s.coefficients()
+        assert np.all(a == 0.0) and np.all(b == 0.0) and np.all(sig == 0.0)
+        if eta > 0.0:
+            s.set_noise(torch.from_numpy(inputs.step_noise(1, T, wl.D).reshape(-1)).cuda())
+        out = s.sample(x).cpu().numpy()
+        st = s.stats()
+    assert np.array_equal(out, x.cpu().numpy())
+    assert st["sweeps"] == -(-T // P) and st["nfe"] == T and st["hits"] == 0
+
+
 @pytest.mark.parametrize("T", [10, 50, 100, 1000])
 def test_uploaded_coefficients_are_rounded_oracle_values(T, gpu_lib):
     wl = W.TINY_LINEAR.with_(T=T, window=min(4, T))

@@ -47,6 +47,26 @@ def test_eta0_is_ddim_and_last_step_is_noise_free():
         assert s1[-1] == 0.0 and np.all(s1[:-1] > 0.0)
 
 
+@pytest.mark.parametrize("eta", [0.0, 0.5, 1.0])
+def test_noiseless_steps_of_degenerate_schedules(eta):
+    """sigma_i = eta x two factors is 0 at eta = 0 and wherever ab_{i+1} = ab_i (the second
+    factor is 0; the first is at most 1, and 0/0 where both are 1): alpha_bar = 1 at every
+    state gives the identity step, alpha = b = sigma = 0, with no NaN; a repeated value
+    below 1 gives sigma = 0 at that step only."""
+    a, b, sig = sch.step_coefficients(np.ones(7), eta)
+    assert np.all(a == 0.0) and np.all(b == 0.0) and np.all(sig == 0.0)
+    ab = np.array([0.2, 0.2, 0.5, 0.5, 1.0])
+    a, b, sig = sch.step_coefficients(ab, eta)
+    assert np.all(np.isfinite(a)) and np.all(np.isfinite(b)) and np.all(np.isfinite(sig))
+    assert sig[0] == 0.0 and sig[2] == 0.0 and a[0] == 0.0 and a[2] == 0.0
+    assert (sig[1] > 0.0) == (eta > 0.0)
+    # eta = 0 is DDIM for any schedule, a decreasing one included (sigma is never formed)
+    dec = np.array([0.9, 0.6, 0.7, 0.3])
+    a0, b0, s0 = sch.step_coefficients(dec, 0.0)
+    ad, bd = sch.ddim_coefficients(dec)
+    assert np.array_equal(a0, ad) and np.array_equal(b0, bd) and np.all(s0 == 0.0)
+
+
 @pytest.mark.parametrize("T", [10, 50])
 @pytest.mark.parametrize("model", ["linear", "mlp"])
 def test_ddpm_window1_is_textbook_ddpm(T, model):
