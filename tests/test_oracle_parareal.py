@@ -81,6 +81,26 @@ def test_exact_prefix_after_k_iterations(model):
             assert not np.array_equal(U[k + 1], ref[k + 1])
 
 
+@pytest.mark.parametrize("T,B", [(20, 4), (12, 3), (10, 10)])
+def test_zero_steps_stop_after_one_iteration(T, B):
+    """The Eq. (2) stop taken literally (every r <= tau): with alpha_bar = 1 at every state
+    both propagators are the identity, the first iteration changes no boundary (r = 0), and
+    at tau = 0 the sampler stops there."""
+    ab = np.ones(T + 1)
+    alpha = np.zeros(T)
+    b = np.zeros(T)
+    x = inputs.x_init((4, 8, 8)).reshape(-1)
+    eps = em.linear_eps(inputs.linear_coefficients(T))
+    xp, trace, st = pr.sample(x, T, B, 0.0, 0.0, ab, alpha, b, eps)
+    assert st["iters"] == 1 and trace[-1]["done"] and np.all(trace[-1]["r"] == 0.0)
+    assert np.array_equal(xp, x.astype(np.float32))
+    # delta = 0, no hits: B coarse requests of the initialization, T fine steps and the B - 1
+    # coarse corrections of blocks 1..B-1
+    assert st["nfe"] == T + 2 * B - 1 and st["hits"] == 0
+    xu, nfe_u, iters_u = pr.uncached(x, T, B, 0.0, ab, alpha, b, eps)
+    assert iters_u == 1 and np.array_equal(xu, xp)
+
+
 def test_initialization_is_coarse_textbook_ddim():
     T, B = 30, 6
     L = T // B

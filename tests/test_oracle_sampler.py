@@ -86,6 +86,29 @@ def test_fixed_point_tau0_is_serial_exactly():
     assert np.max(np.abs(xp - ref)) <= 1e-12 * np.max(np.abs(ref))
 
 
+@pytest.mark.parametrize("T,P", [(10, 4), (12, 3), (7, 7), (9, 1), (30, 8)])
+@pytest.mark.parametrize("delta", [0.0, 0.05])
+def test_zero_drift_converges_in_one_sweep_per_window(T, P, delta):
+    """Eq. (2) taken literally (r <= tau): with zero drift the trajectory is constant, every
+    residual is exactly 0, and at tau = 0 every state of a window counts as converged, so
+    each sweep slides the window to its end: ceil(T / P) sweeps, every step evaluated once.
+    The uncached reference and the scalar simulator agree."""
+    alpha = np.zeros(T)
+    b = np.zeros(T)
+    x = inputs.x_init((4, 8, 8)).reshape(-1)
+    c = inputs.linear_coefficients(T)
+    eps = em.linear_eps(c)
+    xp, tr, st = sp.sample(x, T, P, delta, 0.0, alpha, b, eps)
+    assert np.array_equal(xp, x.astype(np.float32))
+    assert st.sweeps == -(-T // P) and st.nfe == T and st.hits == 0
+    for rec in tr:
+        assert np.all(rec["r"] == 0.0) and rec["s_next"] == rec["e"]
+    xu, tru, nfe_u = sp.picard_uncached(x, T, P, 0.0, alpha, b, eps)
+    assert len(tru) == st.sweeps and nfe_u == T and np.array_equal(xu, xp)
+    sim = scalar_sim.simulate(x, T, P, delta, 0.0, alpha, b, c)
+    assert sim["sweeps"] == st.sweeps and sim["nfe"] == T
+
+
 @pytest.mark.parametrize("model,delta", [("linear", 0.0), ("mlp", 0.0)])
 def test_fixed_point_within_tau(model, delta):
     T, P, tau = 10, 4, 1e-3
