@@ -156,3 +156,20 @@ def test_parareal_repeatable_and_state_errors(gpu_lib):
             s.trace(0)
         assert ei.value.code == B.PA_ERR_STATE          # no trace flag
     assert np.array_equal(a, b_) and st1 == st2
+
+
+@pytest.mark.parametrize("T,Bk", [(20, 4), (12, 3), (10, 10)])
+def test_parareal_identity_steps_stop_after_one_iteration(T, Bk, gpu_lib):
+    """alpha_bar = 1 at every state: coarse and fine steps are the identity, the first
+    iteration moves no boundary (every Eq. (2) residual exactly 0), and at tau = 0 (r <= tau)
+    the sampler stops there: one iteration, NFE = T + 2B - 1 at delta = 0 (the B coarse
+    requests of the initialization, T fine steps, B - 1 coarse corrections), the initial
+    latent returned bit for bit."""
+    wl = Workload(f"pr_identity_T{T}_B{Bk}", (4, 8, 8), T, 1, 0.0, 0.0, "linear", blocks=Bk)
+    sched = {"alpha_bar": np.ones(T + 1), "t_values": sch.trailing_timesteps(T)}
+    x = torch.from_numpy(inputs.x_init(wl.latent).reshape(-1)).cuda()
+    with B.parareal_from_workload(wl, 0.0, schedule=sched) as s:
+        out = s.sample(x).cpu().numpy()
+        st = s.stats()
+    assert np.array_equal(out, x.cpu().numpy())
+    assert st["iterations"] == 1 and st["done"] == 1 and st["nfe"] == T + 2 * Bk - 1 and st["hits"] == 0
