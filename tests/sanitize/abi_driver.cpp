@@ -293,6 +293,9 @@ void run_handle(const int32_t shape[4], int T, int window, const pa_schedule_t& 
         EXPECT(tr->m > 0);
         EXPECT_RC(paraanya_trace_sample(h, N - 1, 0, tr), PA_OK);
         EXPECT_RC(paraanya_trace(h, sweeps + 5, tr), PA_ERR_INVALID_ARG);
+        EXPECT_RC(paraanya_trace(h, -1, tr), PA_ERR_INVALID_ARG);
+        EXPECT_RC(paraanya_trace_sample(h, N, 0, tr), PA_ERR_INVALID_ARG);
+        EXPECT_RC(paraanya_trace(h, 0, nullptr), PA_ERR_INVALID_ARG);
     } else {
         EXPECT_RC(paraanya_trace(h, 0, tr), PA_ERR_STATE);
     }
@@ -302,6 +305,10 @@ void run_handle(const int32_t shape[4], int T, int window, const pa_schedule_t& 
     for (size_t i = (size_t)T * D; i < X.size(); ++i) EXPECT(isfinite(X[i]));
     EXPECT_RC(paraanya_read_state_sample(h, N - 1, T - 1, T + 1, X.data(), nullptr, nullptr, nullptr), PA_OK);
     EXPECT_RC(paraanya_read_state(h, 0, T + 2, X.data(), nullptr, nullptr, nullptr), PA_ERR_INVALID_ARG);
+    EXPECT_RC(paraanya_read_state(h, -1, 1, X.data(), nullptr, nullptr, nullptr), PA_ERR_INVALID_ARG);
+    EXPECT_RC(paraanya_read_state(h, 2, 1, X.data(), nullptr, nullptr, nullptr), PA_ERR_INVALID_ARG);
+    EXPECT_RC(paraanya_read_state(h, 1, 1, X.data(), Xh.data(), Eh.data(), valid.data()), PA_OK);   // empty
+    EXPECT_RC(paraanya_read_state_sample(h, -1, 0, 1, X.data(), nullptr, nullptr, nullptr), PA_ERR_INVALID_ARG);
     std::vector<double> a(T), b(T), s(T);
     std::vector<float> temb(m.em.kind == PA_EPS_PATCH_MLP ? (size_t)T * m.em.hidden : 1);
     EXPECT_RC(paraanya_coefficients(h, a.data(), b.data(), s.data(),
