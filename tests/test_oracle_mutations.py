@@ -54,6 +54,14 @@ MUTATIONS = [
     ("mlp_second_gelu_dropped", "eps_models.py", "h2 = bf16_round(gelu(pre2).astype(F32)).astype(F64)",
      "h2 = bf16_round(pre2.astype(F32)).astype(F64)"),
     ("linear_step_index", "eps_models.py", "c64[np.asarray(steps)]", "c64[np.asarray(steps) - 1]"),
+    ("unpatchify_dh_dw_swapped", "eps_models.py", "t = tok.reshape(H // p, W // p, C, p, p).transpose(2, 0, 3, 1, 4)",
+     "t = tok.reshape(H // p, W // p, C, p, p).transpose(2, 0, 4, 1, 3)"),
+    # the references the pins compare against
+    ("scalar_recurrence_cached_state", "scalar_sim.py", "run += alpha[t] * g[t] + b[t] * c[t] * gh[t]",
+     "run += alpha[t] * gh[t] + b[t] * c[t] * gh[t]"),
+    ("uncached_slide_takes_last_state", "sampler.py", "while c < e - s - 1 and r[c] <= tau:",
+     "while c < e - s and r[c] <= tau:"),
+    ("textbook_ddpm_variance", "sampler.py", "var = beta * (1.0 - ab[i + 1]) / (1.0 - ab[i])", "var = beta"),
     # the cached Picard sampler
     ("picard_anchor", "sampler.py", "    acc = X[s].astype(F64)\n    Y = np.empty((e - s, X.shape[1]), dtype=X.dtype)",
      "    acc = X[s + 1].astype(F64)\n    Y = np.empty((e - s, X.shape[1]), dtype=X.dtype)"),
