@@ -455,3 +455,67 @@ def test_chained_samples_are_stream_ordered(wl, gpu_lib):
             results.append(a.cpu().numpy())
     assert np.array_equal(results[0], results[1])
     assert np.isfinite(results[0]).all()
+
+
+def test_concurrent_handles_on_separate_streams_and_threads(gpu_lib):
+    """Handles share no state: two host threads, each with its own handle on its own stream
+    (default priority), and a third calling the allocation-free entry point (which shares one
+    locked workspace per device) run at the same time; every output and counter equals the
+    same calls made one after another on the current stream."""
+    import threading
+    jobs = [(W.SD_MLP, 1), (W.SMALL_MLP, 2), (W.TINY_LINEAR, 3)]
+    reps = 4
+
+    def xs(wl, n):
+        a = inputs.x_init(wl.latent).reshape(-1) if n == 1 else inputs.x_init_batch(wl.latent, n).reshape(-1)
+        return torch.from_numpy(a)
+
+    def chain(wl, n, stream=None):
+        out, sts = [], []
+        with B.from_workload(wl, batch=n, stream=stream) as s:
+            x = xs(wl, n).cuda()
+            for _ in range(reps):
+                x = s.sample(x)
+                out.append(x.cpu().numpy())
+                sts.append(s.stats())
+        return out, sts
+
+    def noalloc_chain(stream=None):
+        out = []
+        x = xs(W.SMALL_MLP, 1).cuda()
+        for _ in range(reps):
+            x, st = B.sample_noalloc_workload(W.SMALL_MLP, x, stream=stream)
+            out.append((x.cpu().numpy(), st))
+        return out
+
+    ref = [chain(wl, n) for wl, n in jobs]
+    ref_na = noalloc_chain()
+    torch.cuda.synchronize()
+
+    results, errors = {}, []
+
+    def run(key, fn):
+        try:
+            st = torch.cuda.Stream()
+            with torch.cuda.stream(st):
+                results[key] = fn(st)
+                st.synchronize()
+        except Exception as e:      # reported below, in the test's thread
+            errors.append((key, repr(e)))
+
+    threads = [threading.Thread(target=run, args=(i, lambda st, wl=wl, n=n: chain(wl, n, st)))
+               for i, (wl, n) in enumerate(jobs)]
+    threads.append(threading.Thread(target=run, args=("na", lambda st: noalloc_chain(st))))
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads), "a thread did not finish"
+    assert not errors, errors
+    for i in range(len(jobs)):
+        out, sts = results[i]
+        for a, b in zip(out, ref[i][0]):
+            assert np.array_equal(a, b), jobs[i][0].name
+        assert sts == ref[i][1]
+    for (a, sa), (b, sb) in zip(results["na"], ref_na):
+        assert np.array_equal(a, b) and sa == sb
