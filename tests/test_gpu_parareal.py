@@ -45,6 +45,10 @@ CASES = [
     ("lin_c5_shape", _wl("pr_lin_4x96x96_T100_B10", (4, 96, 96), 100, 10), 0.05),
     ("lin_max_blocks", _wl("pr_lin_4x8x8_T64_B64", (4, 8, 8), 64, 64), 0.05),
     ("mlp_small", _wl("pr_mlp_4x32x32_T20_B4_H512", (4, 32, 32), 20, 4, "patch_mlp", 512), 0.05),
+    # the most blocks, two fine steps each: fine-step launches of up to 64 latents through the
+    # network kernel, over several iterations (all misses at delta = 0)
+    ("mlp_max_blocks", _wl("pr_mlp_4x16x32_T128_B64_H512", (4, 16, 32), 128, 64, "patch_mlp", 512), 0.05),
+    ("mlp_max_blocks_delta0", _wl("pr_mlp_4x16x32_T128_B64_H512", (4, 16, 32), 128, 64, "patch_mlp", 512), 0.0),
     ("mlp_c5", W.PARAREAL_MLP, 0.05),
     ("mlp_c5_delta0", W.PARAREAL_MLP, 0.0),
 ]
