@@ -519,3 +519,22 @@ def test_concurrent_handles_on_separate_streams_and_threads(gpu_lib):
         assert sts == ref[i][1]
     for (a, sa), (b, sb) in zip(results["na"], ref_na):
         assert np.array_equal(a, b) and sa == sb
+
+
+@pytest.mark.parametrize("wl,batch,reps", [(W.SD_MLP, 1, 200), (W.SD_MLP, 8, 40), (W.TINY_LINEAR, 5, 300)])
+def test_repeated_samples_are_bitwise_identical(wl, batch, reps, gpu_lib):
+    """Soak for races: many samples back to back on one handle (each returning before its
+    output copy has run, the counters taken from the final progress and counter words) give
+    the same output bits and counters every time."""
+    xs = inputs.x_init(wl.latent).reshape(-1) if batch == 1 else inputs.x_init_batch(wl.latent, batch).reshape(-1)
+    x = torch.from_numpy(xs).cuda()
+    with B.from_workload(wl, batch=batch) as s:
+        outs = [torch.empty_like(x) for _ in range(reps)]
+        stats = []
+        for o in outs:
+            s.sample(x, o)
+            stats.append(s.stats())
+        first = outs[0].cpu().numpy()
+        for i, o in enumerate(outs):
+            assert np.array_equal(o.cpu().numpy(), first), f"sample {i} differs"
+    assert all(st == stats[0] for st in stats)
