@@ -177,3 +177,17 @@ def test_parareal_identity_steps_stop_after_one_iteration(T, Bk, gpu_lib):
         st = s.stats()
     assert np.array_equal(out, x.cpu().numpy())
     assert st["iterations"] == 1 and st["done"] == 1 and st["nfe"] == T + 2 * Bk - 1 and st["hits"] == 0
+
+
+def test_parareal_repeated_samples_are_bitwise_identical(gpu_lib):
+    """Soak for races: 20 Parareal samples back to back at the full 4x96x96, H = 2048 shape
+    give the same output bits and counters every time."""
+    wl = W.PARAREAL_MLP
+    x = torch.from_numpy(inputs.x_init(wl.latent).reshape(-1)).cuda()
+    with B.parareal_from_workload(wl, 0.05) as s:
+        outs, stats = [], []
+        for _ in range(20):
+            outs.append(s.sample(x).cpu().numpy())
+            stats.append(s.stats())
+    assert all(np.array_equal(o, outs[0]) for o in outs)
+    assert all(st == stats[0] for st in stats)
