@@ -23,6 +23,9 @@ Beside the headline line (same JSON object, extra keys):
   picard_beyond_cache  the solver kernels at 64 samples per handle of the same workload: one
                      Picard launch then touches ~0.5 GB, more than the 256 MB Infinity Cache,
                      so its rate is that of HBM (the one- and eight-sample figures are not).
+  shard_share        one GPU's share of a sweep's misses if they were split over G GPUs: the
+                     network launch with 32 / G misses at the same shape (window 32 / G at
+                     delta = 0, so every launch evaluates that many latents), G in {1, 2, 4, 8}.
 
 Prints one JSON line (rank 0). Throughput figures (value, ms_per_step, ε evals/s, and those of
 the extra measurements) come from samples launched exactly as a user launches them, with no
@@ -106,7 +109,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--headline-only", action="store_true",
                     help="skip the revisit, batched, DDPM and Parareal measurements")
-    ap.add_argument("--extras", type=str, default="revisit,batched,ddpm,long,parareal,hbm",
+    ap.add_argument("--extras", type=str, default="revisit,batched,ddpm,long,parareal,hbm,shard",
                     help="which extra measurements to run (comma list)")
     ap.add_argument("--cpu-seconds", type=float, default=6.0,
                     help="budget of each of the oracle's two bounded samples (all threads, one)")
@@ -399,6 +402,20 @@ def main():
             "samples": nh, "delta": PRIMARY_DELTA, "steps": 2, "solver_kernels": sk}
         print(f"[bench] picard at batch {nh}: {sk['k_picard']['bytes_per_launch'] / 1e6:.0f} MB/launch, "
               f"{sk['k_picard']['achieved']:.0f} GB/s", file=sys.stderr, flush=True)
+    if not args.headline_only and "shard" in want:
+        # the network kernel on one GPU's share of the misses (m / G latents per launch)
+        fpe = flops_per_eval(wl)
+        share = {}
+        for G in (1, 2, 4, 8):
+            ws = wl.with_(window=wl.window // G)
+            r = run_case(ws, 0.0, max(args.steps // 40, 3), 1, torch, weights)
+            per = r["eps_ms"] * 1e3 / max(r["launches"], 1)
+            m = r["profiled_nfe"] / max(r["launches"], 1)
+            share[str(G)] = {"misses_per_launch": m, "avg_launch_us": per,
+                             "tflops": m * fpe / (per * 1e-6) / 1e12 if per > 0 else None}
+            print(f"[bench] shard share G={G}: {m:.1f} misses/launch, {per:.1f} us/launch",
+                  file=sys.stderr, flush=True)
+        extras["shard_share"] = {"workload": wl.name, "delta": 0.0, "per_G": share}
     if not args.headline_only and "ddpm" in want:
         # the window study's stochastic setting
         wd = wl.with_(T=1000, window=64)
